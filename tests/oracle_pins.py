@@ -1,0 +1,338 @@
+"""Pins that tie the CPU oracle to facts fixed by the paper and by mathematics.
+
+Each pin is a function `pin_x(lib)` that raises AssertionError when the oracle
+loaded as `lib` disagrees with a fact that does not come from the oracle:
+hand-derived closed forms (tests/golden/hand_cases.yaml), closed forms for
+zero queries, reductions between variants, probability invariants, and the
+fp64 library routine torch.nn.functional.scaled_dot_product_attention.
+
+The same pins run against deliberately broken copies of the oracle
+(test_oracle_mutants.py) to show that a plausible mistake fails at least one.
+"""
+from __future__ import annotations
+
+import math
+import os
+
+import numpy as np
+import torch
+import torch.nn.functional as F
+import yaml
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_cases.yaml")
+_NS = {"ln": math.log, "exp": math.exp, "e": math.e, "inf": math.inf, "sqrt": math.sqrt}
+_MASKS = {"none": oracle.MASK_NONE, "causal": oracle.MASK_CAUSAL,
+          "window": oracle.MASK_SLIDING_WINDOW}
+
+
+def _val(x):
+    if isinstance(x, list):
+        return [_val(y) for y in x]
+    if isinstance(x, (int, float)):
+        return float(x)
+    return float(eval(str(x), {"__builtins__": {}}, _NS))  # fixture arithmetic only
+
+
+def _close(a, b, tol, what):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    assert a.shape == b.shape, f"{what}: shape {a.shape} vs {b.shape}"
+    inf_a, inf_b = np.isinf(a), np.isinf(b)
+    assert np.array_equal(inf_a, inf_b) and np.array_equal(a[inf_a], b[inf_b]), \
+        f"{what}: infinities differ\n{a}\n{b}"
+    fin = ~inf_a
+    err = np.max(np.abs(a[fin] - b[fin])) if fin.any() else 0.0
+    assert err <= tol, f"{what}: max abs err {err:.3e} > {tol:.1e}\n{a}\n{b}"
+
+
+def load_hand_cases():
+    with open(GOLDEN) as f:
+        return yaml.safe_load(f)["cases"]
+
+
+def _run_case(lib, c):
+    q = np.array(_val(c["q"]), dtype=np.float32)
+    k = np.array(_val(c["k"]), dtype=np.float32)
+    v = np.array(_val(c["v"]), dtype=np.float32)
+    kw = dict(scale=_val(c["scale"]), mask=_MASKS[c["mask"]],
+              window_left=int(c.get("window_left", -1)),
+              window_right=int(c.get("window_right", -1)),
+              softcap=_val(c.get("softcap", 0)), lib=lib)
+    if "slopes" in c:
+        kw["slopes"] = np.array(_val(c["slopes"]), dtype=np.float32)
+    if "cu" in c:
+        cu = np.array(c["cu"], dtype=np.int32)
+        o, lse = oracle.attention(q[:, None, :], k[:, None, :], v[:, None, :],
+                                  cu_seqlens_q=cu, cu_seqlens_k=cu, **kw)
+        return o[:, 0, :], lse[0]
+    if "heads" in c:
+        o, lse = oracle.attention(q[None], k[None], v[None], **kw)
+        return o[0], lse[0]
+    o, lse = oracle.attention(q[None, None], k[None, None], v[None, None], **kw)
+    return o[0, 0], lse[0, 0]
+
+
+def pin_hand_cases(lib):
+    """Every hand-derived case (inputs are fp32, so allow fp32 input rounding)."""
+    for c in load_hand_cases():
+        o, lse = _run_case(lib, c)
+        _close(o, _val(c["o"]), 2e-6, c["name"] + " O")
+        _close(lse, _val(c["lse"]), 2e-6, c["name"] + " LSE")
+
+
+def _rand(shape, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(shape, generator=g, dtype=torch.float32) * scale)
+
+
+def pin_probability_rows(lib):
+    """Rows of P sum to one and P = exp(score - LSE) is consistent with O = P V."""
+    B, H, S, D = 2, 3, 9, 5
+    q, k, v = _rand((B, H, S, D), 1), _rand((B, H, S, D), 2), _rand((B, H, S, D), 3)
+    slopes = torch.tensor([0.5, 0.25, 0.125])
+    for kw in (dict(mask=oracle.MASK_NONE), dict(mask=oracle.MASK_CAUSAL),
+               dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=2, window_right=1),
+               dict(mask=oracle.MASK_NONE, softcap=1.5, slopes=slopes)):
+        o, lse, p = oracle.attention(q, k, v, scale=0.4, want_probs=True, lib=lib, **kw)
+        _close(p.sum(-1), np.ones((B, H, S)), 1e-12, f"row sums {kw}")
+        assert (p >= 0).all()
+        _close(o, np.einsum("bhij,bhjd->bhid", p, v.double().numpy()), 1e-12, f"O = P V {kw}")
+
+
+def pin_constant_v(lib):
+    """Constant V = c gives O = c whatever the scores."""
+    B, H, S, D = 1, 2, 7, 4
+    q, k = _rand((B, H, S, D), 4, 2.0), _rand((B, H, S, D), 5, 2.0)
+    v = torch.full((B, H, S, D), -1.75)
+    for kw in (dict(mask=oracle.MASK_NONE, softcap=3.0),
+               dict(mask=oracle.MASK_CAUSAL, slopes=torch.tensor([0.3, 1.1])),
+               dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=1, window_right=0)):
+        o, _ = oracle.attention(q, k, v, scale=0.7, lib=lib, **kw)
+        _close(o, np.full((B, H, S, D), -1.75), 1e-12, f"constant V {kw}")
+
+
+def pin_causal_row0(lib):
+    """Causal row 0 sees only key 0: O_0 = V_0, LSE_0 = scale * q_0 . k_0."""
+    B, H, S, D = 2, 2, 6, 8
+    q, k, v = _rand((B, H, S, D), 6), _rand((B, H, S, D), 7), _rand((B, H, S, D), 8)
+    o, lse = oracle.attention(q, k, v, scale=0.3, mask=oracle.MASK_CAUSAL, lib=lib)
+    _close(o[:, :, 0], v[:, :, 0].double().numpy(), 1e-12, "causal O_0")
+    s00 = 0.3 * (q[:, :, 0].double() * k[:, :, 0].double()).sum(-1)
+    _close(lse[:, :, 0], s00.numpy(), 1e-12, "causal LSE_0")
+
+
+def pin_single_key_window(lib):
+    """window_left = window_right = 0: each row sees only its own key."""
+    B, H, S, D = 1, 2, 5, 3
+    q, k, v = _rand((B, H, S, D), 9), _rand((B, H, S, D), 10), _rand((B, H, S, D), 11)
+    o, lse = oracle.attention(q, k, v, scale=1.3, mask=oracle.MASK_SLIDING_WINDOW,
+                              window_left=0, window_right=0, lib=lib)
+    _close(o, v.double().numpy(), 1e-12, "window 0 O")
+    _close(lse, (1.3 * (q.double() * k.double()).sum(-1)).numpy(), 1e-12, "window 0 LSE")
+
+
+def pin_zero_query_counts(lib):
+    """Q = 0: O_i = mean of visible V rows, LSE_i = ln(n_i), n_i from the mask."""
+    S, D = 11, 3
+    v = _rand((1, 1, S, D), 12)
+    q = torch.zeros((1, 1, S, D))
+    k = _rand((1, 1, S, D), 13)
+    vn = v[0, 0].double().numpy()
+    cases = [
+        (dict(mask=oracle.MASK_NONE), lambda i: (0, S - 1)),
+        (dict(mask=oracle.MASK_CAUSAL), lambda i: (0, i)),
+        (dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=3, window_right=0),
+         lambda i: (max(0, i - 3), i)),
+        (dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=2, window_right=4),
+         lambda i: (max(0, i - 2), min(S - 1, i + 4))),
+        (dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=-1, window_right=2),
+         lambda i: (0, min(S - 1, i + 2))),
+    ]
+    for kw, rng in cases:
+        o, lse = oracle.attention(q, k, v, scale=1.0, lib=lib, **kw)
+        for i in range(S):
+            a, b = rng(i)
+            _close(o[0, 0, i], vn[a:b + 1].mean(0), 1e-12, f"Q=0 O row {i} {kw}")
+            _close(lse[0, 0, i], math.log(b - a + 1), 1e-12, f"Q=0 LSE row {i} {kw}")
+    # bottom-right causal with Sq < Sk: query i sits at key position i + Sk - Sq
+    sq = 4
+    o, lse = oracle.attention(q[:, :, :sq], k, v, scale=1.0, mask=oracle.MASK_CAUSAL, lib=lib)
+    for i in range(sq):
+        n = i + S - sq + 1
+        _close(o[0, 0, i], vn[:n].mean(0), 1e-12, f"bottom-right O row {i}")
+        _close(lse[0, 0, i], math.log(n), 1e-12, f"bottom-right LSE row {i}")
+
+
+def pin_zero_query_alibi(lib):
+    """Q = 0 with ALiBi: weights r^|i-j| (r = e^-m), a two-sided geometric sum.
+
+    With V = identity (D = S), O_i[j] = r^|i-j| / Z_i and
+    Z_i = (1 - r^(i+1))/(1 - r) + r (1 - r^(S-1-i))/(1 - r)."""
+    S = 9
+    m = 0.37
+    r = math.exp(-m)
+    q = torch.zeros((1, 1, S, S))
+    k = _rand((1, 1, S, S), 14)
+    v = torch.eye(S).reshape(1, 1, S, S)
+    o, lse = oracle.attention(q, k, v, scale=1.0, slopes=torch.tensor([m]), lib=lib)
+    for i in range(S):
+        z = (1 - r ** (i + 1)) / (1 - r) + r * (1 - r ** (S - 1 - i)) / (1 - r)
+        _close(lse[0, 0, i], math.log(z), 1e-6, f"ALiBi Z row {i}")
+        _close(o[0, 0, i], [r ** abs(i - j) / z for j in range(S)], 1e-6, f"ALiBi O row {i}")
+    # causal: only j <= i, Z_i = (1 - r^(i+1)) / (1 - r)
+    o, lse = oracle.attention(q, k, v, scale=1.0, mask=oracle.MASK_CAUSAL,
+                              slopes=torch.tensor([m]), lib=lib)
+    for i in range(S):
+        z = (1 - r ** (i + 1)) / (1 - r)
+        _close(lse[0, 0, i], math.log(z), 1e-6, f"causal ALiBi Z row {i}")
+
+
+def pin_reductions(lib):
+    """window >= Sk-1 is causal; C = 1e4 is (almost) no cap; zero slopes are no ALiBi."""
+    B, H, S, D = 1, 2, 16, 8
+    q, k, v = _rand((B, H, S, D), 15), _rand((B, H, S, D), 16), _rand((B, H, S, D), 17)
+    oc, lc = oracle.attention(q, k, v, scale=0.35, mask=oracle.MASK_CAUSAL, lib=lib)
+    for wl in (S - 1, S + 5, -1):
+        ow, lw = oracle.attention(q, k, v, scale=0.35, mask=oracle.MASK_SLIDING_WINDOW,
+                                  window_left=wl, window_right=0, lib=lib)
+        _close(ow, oc, 0.0, f"window {wl} == causal O")
+        _close(lw, lc, 0.0, f"window {wl} == causal LSE")
+    op, lp = oracle.attention(q, k, v, scale=0.35, lib=lib)
+    # |C tanh(s/C) - s| <= |s|^3 / (3 C^2); |s| < 5 here, so the gap is < 5e-7
+    ocap, lcap = oracle.attention(q, k, v, scale=0.35, softcap=1e4, lib=lib)
+    _close(ocap, op, 1e-6, "softcap 1e4 O")
+    _close(lcap, lp, 1e-6, "softcap 1e4 LSE")
+    oz, lz = oracle.attention(q, k, v, scale=0.35, slopes=torch.zeros(H), lib=lib)
+    _close(oz, op, 0.0, "zero slopes O")
+    _close(lz, lp, 0.0, "zero slopes LSE")
+
+
+def pin_torch_sdpa(lib):
+    """fp64 torch SDPA (library routine): plain, causal, GQA, window and ALiBi masks."""
+    B, Hq, Hkv, S, D = 2, 4, 2, 13, 6
+    q = _rand((B, Hq, S, D), 18, 1.5).double()
+    k = _rand((B, Hkv, S, D), 19, 1.5).double()
+    v = _rand((B, Hkv, S, D), 20).double()
+    sc = 0.45
+    # plain and causal with grouped-query heads (torch repeats kv heads in contiguous groups)
+    for causal in (False, True):
+        ref = F.scaled_dot_product_attention(q, k, v, is_causal=causal, scale=sc, enable_gqa=True)
+        o, _ = oracle.attention(q, k, v, scale=sc, lib=lib,
+                                mask=oracle.MASK_CAUSAL if causal else oracle.MASK_NONE)
+        _close(o, ref.numpy(), 1e-12, f"sdpa causal={causal}")
+    kr = k.repeat_interleave(Hq // Hkv, dim=1)
+    vr = v.repeat_interleave(Hq // Hkv, dim=1)
+    # band mask from torch's triangular routines: keys i-3 .. i+1 visible
+    band = torch.ones(S, S, dtype=torch.bool).tril(1).triu(-3)
+    ref = F.scaled_dot_product_attention(q, kr, vr, attn_mask=band, scale=sc)
+    o, _ = oracle.attention(q, k, v, scale=sc, mask=oracle.MASK_SLIDING_WINDOW,
+                            window_left=3, window_right=1, lib=lib)
+    _close(o, ref.numpy(), 1e-12, "sdpa band")
+    # ALiBi as an additive float mask: -slope_h * |i - j|
+    slopes = torch.tensor([0.5, 0.25, 0.125, 0.0625], dtype=torch.float64)
+    idx = torch.arange(S, dtype=torch.float64)
+    dist = (idx[:, None] - idx[None, :]).abs()
+    bias = -slopes[:, None, None] * dist[None]
+    ref = F.scaled_dot_product_attention(q, kr, vr, attn_mask=bias[None], scale=sc)
+    o, lse = oracle.attention(q, k, v, scale=sc, slopes=slopes.float(), lib=lib)
+    _close(o, ref.numpy(), 1e-12, "sdpa alibi")
+    # LSE against torch.logsumexp of the same biased scores
+    s = sc * torch.einsum("bhid,bhjd->bhij", q, kr) + bias[None]
+    _close(lse, torch.logsumexp(s, -1).numpy(), 1e-12, "logsumexp alibi")
+
+
+def pin_gqa_equals_repeated(lib):
+    """GQA equals MHA over K/V heads repeated in contiguous groups."""
+    B, Hq, Hkv, S, D = 1, 6, 2, 10, 4
+    q, k, v = _rand((B, Hq, S, D), 21), _rand((B, Hkv, S, D), 22), _rand((B, Hkv, S, D), 23)
+    kw = dict(scale=0.5, mask=oracle.MASK_SLIDING_WINDOW, window_left=4, window_right=0,
+              softcap=2.5, slopes=torch.linspace(0.1, 0.6, Hq), lib=lib)
+    og, lg = oracle.attention(q, k, v, **kw)
+    om, lm = oracle.attention(q, k.repeat_interleave(3, 1), v.repeat_interleave(3, 1), **kw)
+    _close(og, om, 0.0, "GQA O")
+    _close(lg, lm, 0.0, "GQA LSE")
+
+
+def pin_varlen_concat(lib):
+    """Varlen equals independent fixed-length runs per sequence (incl. empty ones)."""
+    lens = [5, 0, 1, 9, 3]
+    Hq, Hkv, D = 4, 2, 6
+    T = sum(lens)
+    q, k, v = _rand((T, Hq, D), 24), _rand((T, Hkv, D), 25), _rand((T, Hkv, D), 26)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    slopes = torch.tensor([0.2, 0.4, 0.6, 0.8])
+    for kw in (dict(mask=oracle.MASK_CAUSAL),
+               dict(mask=oracle.MASK_NONE, slopes=slopes, softcap=3.0),
+               dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=2, window_right=0)):
+        ov, lv = oracle.attention(q, k, v, scale=0.6, cu_seqlens_q=cu, cu_seqlens_k=cu,
+                                  lib=lib, **kw)
+        for s, n in enumerate(lens):
+            if n == 0:
+                continue
+            a = cu[s]
+            sl = slice(a, a + n)
+            of, lf = oracle.attention(q[sl].permute(1, 0, 2)[None], k[sl].permute(1, 0, 2)[None],
+                                      v[sl].permute(1, 0, 2)[None], scale=0.6, lib=lib, **kw)
+            _close(ov[sl], of[0].transpose(1, 0, 2), 0.0, f"varlen O seq {s} {kw}")
+            _close(lv[:, sl], lf[0], 0.0, f"varlen LSE seq {s} {kw}")
+
+
+def pin_varlen_unequal_lengths(lib):
+    """Varlen with separate query/key lengths, Q = 0: bottom-right causal per sequence.
+
+    Query i of a sequence with Lq queries and Lk keys sees keys 0..i+Lk-Lq, so
+    n_i = clip(i + Lk - Lq + 1, 0, Lk); O_i is the mean of those V rows and
+    LSE_i = ln n_i (an empty row has O = 0, LSE = -inf)."""
+    lq = [3, 4, 2, 0, 2]
+    lk = [5, 2, 0, 3, 2]
+    cuq = np.concatenate([[0], np.cumsum(lq)]).astype(np.int32)
+    cuk = np.concatenate([[0], np.cumsum(lk)]).astype(np.int32)
+    D = 2
+    q = torch.zeros((sum(lq), 1, D))
+    k = _rand((sum(lk), 1, D), 30)
+    v = _rand((sum(lk), 1, D), 31)
+    o, lse = oracle.attention(q, k, v, scale=1.0, mask=oracle.MASK_CAUSAL,
+                              cu_seqlens_q=cuq, cu_seqlens_k=cuk, lib=lib)
+    vn = v[:, 0].double().numpy()
+    for s_, (a, b) in enumerate(zip(lq, lk)):
+        for i in range(a):
+            n = min(max(i + b - a + 1, 0), b)
+            t = cuq[s_] + i
+            if n == 0:
+                _close(o[t, 0], np.zeros(D), 0.0, f"empty row seq {s_} i {i}")
+                _close(lse[0, t], -math.inf, 0.0, f"empty LSE seq {s_} i {i}")
+            else:
+                _close(o[t, 0], vn[cuk[s_]:cuk[s_] + n].mean(0), 1e-12, f"O seq {s_} i {i}")
+                _close(lse[0, t], math.log(n), 1e-12, f"LSE seq {s_} i {i}")
+
+
+def pin_row_subset(lib):
+    """Computing a subset of rows gives the same values as computing all rows."""
+    B, H, S, D = 2, 3, 7, 4
+    q, k, v = _rand((B, H, S, D), 27), _rand((B, H, S, D), 28), _rand((B, H, S, D), 29)
+    o, lse = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_CAUSAL, lib=lib)
+    rows = [0, 5, 17, 41]
+    os_, ls = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_CAUSAL, rows=rows, lib=lib)
+    flat_o, flat_os = o.reshape(-1, D), os_.reshape(-1, D)
+    _close(flat_os[rows], flat_o[rows], 0.0, "row subset O")
+    _close(ls.reshape(-1)[rows], lse.reshape(-1)[rows], 0.0, "row subset LSE")
+    assert np.isnan(np.delete(ls.reshape(-1), rows)).all()
+
+
+ALL_PINS = [pin_hand_cases, pin_probability_rows, pin_constant_v, pin_causal_row0,
+            pin_single_key_window, pin_zero_query_counts, pin_zero_query_alibi,
+            pin_reductions, pin_torch_sdpa, pin_gqa_equals_repeated, pin_varlen_concat,
+            pin_varlen_unequal_lengths, pin_row_subset]
+
+
+def failing_pins(lib):
+    """Names of the pins that fail for `lib` (empty when all hold)."""
+    bad = []
+    for pin in ALL_PINS:
+        try:
+            pin(lib)
+        except (AssertionError, ValueError) as e:  # noqa: PERF203
+            bad.append((pin.__name__, str(e).splitlines()[0] if str(e) else ""))
+    return bad

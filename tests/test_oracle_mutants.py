@@ -1,0 +1,50 @@
+"""Plant plausible mistakes in copies of the oracle and check the pins catch each.
+
+Every mutant is a textual edit of oracle/attn_ref.c compiled into a temporary
+directory; the oracle itself is never modified. A mutant that passes every pin
+would mean the pins cannot tell that mistake from the truth.
+"""
+import os
+
+import pytest
+
+import oracle
+import oracle_pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "attn_ref.c")
+
+MUTANTS = [
+    ("scale dropped", "double s = p->scale * dot;", "double s = dot;"),
+    ("softcap missing outer C", "s = p->softcap * tanh(s / p->softcap);", "s = tanh(s / p->softcap);"),
+    ("softcap after ALiBi", "if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);\n    if (p->slopes) {\n        int64_t rel = i + (lk - lq) - j;\n        s -= p->slopes[h] * (double)(rel < 0 ? -rel : rel);\n    }",
+     "if (p->slopes) {\n        int64_t rel = i + (lk - lq) - j;\n        s -= p->slopes[h] * (double)(rel < 0 ? -rel : rel);\n    }\n    if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);"),
+    ("ALiBi sign", "s -= p->slopes[h]", "s += p->slopes[h]"),
+    ("ALiBi signed distance", "(double)(rel < 0 ? -rel : rel)", "(double)rel"),
+    ("ALiBi slope of kv head", "s -= p->slopes[h]", "s -= p->slopes[h / (p->hq / p->hkv)]"),
+    ("causal strict", "if (p->mask_kind == 1) return j <= ii;", "if (p->mask_kind == 1) return j < ii;"),
+    ("causal top-left", "int64_t ii = i + (lk - lq); /* query position", "int64_t ii = i; /* query position"),
+    ("window left off by one", "ii - j > p->window_left", "ii - j >= p->window_left"),
+    ("window right ignored", "if (p->window_right >= 0 && j - ii > p->window_right) return 0;", ""),
+    ("GQA modulo map", "int32_t hk = h / group;", "int32_t hk = h % p->hkv;"),
+    ("LSE without max", "lse[row] = mx + log(z);", "lse[row] = log(z);"),
+    ("no normalisation", "double pj = exp(s[j] - mx) / z;", "double pj = exp(s[j] - mx);"),
+    ("sum without max shift", "z += exp(s[j] - mx);", "z += exp(s[j]);"),
+    ("V used as K", "score(p, qi, kbase + j * kstride", "score(p, qi, vbase + j * kstride"),
+    ("varlen keys from sequence 0", "kbase = k + ((int64_t)p->cu_k[b] * p->hkv + hk) * p->d;",
+     "kbase = k + ((int64_t)0 * p->hkv + hk) * p->d;"),
+    ("varlen key length from queries", "lk = p->cu_k[b + 1] - p->cu_k[b];", "lk = lq;"),
+    ("empty row LSE zero", "lse[row] = -INFINITY;", "lse[row] = 0.0;"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation site for '{name}' not found"
+    mutated = src.replace(old, new)
+    path = tmp_path / "attn_ref_mutant.c"
+    path.write_text(mutated)
+    so = oracle.build(str(path), str(tmp_path / "libmutant.so"))
+    lib = oracle.load(so)
+    failed = oracle_pins.failing_pins(lib)
+    assert failed, f"no pin catches the mutant '{name}'"
