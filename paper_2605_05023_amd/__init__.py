@@ -1,0 +1,108 @@
+"""MI355X (gfx950) fused attention forward.
+
+`fwd` marshals torch tensors (device memory and the current stream) into an
+`attn_variant_desc` and calls `attn_fwd` of libattn.so. The computation runs
+entirely in the library's HIP kernels; if the library is missing the import
+of `fwd`'s backend fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from typing import Optional
+
+import torch
+
+from ._abi import (ATTN_BF16, ATTN_FP32, ATTN_MASK_CAUSAL, ATTN_MASK_NONE,  # noqa: F401
+                   ATTN_MASK_SLIDING_WINDOW, AttnError, AttnVariantDesc, check, load, plan_tiles)
+
+__all__ = ["fwd", "make_desc", "AttnError", "AttnVariantDesc", "load", "plan_tiles",
+           "ATTN_BF16", "ATTN_FP32", "ATTN_MASK_NONE", "ATTN_MASK_CAUSAL",
+           "ATTN_MASK_SLIDING_WINDOW"]
+
+_DTYPES = {torch.bfloat16: ATTN_BF16, torch.float32: ATTN_FP32}
+
+
+def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, softcap=0.0,
+              scale=None, cu_seqlens_q=None, cu_seqlens_k=None, max_seqlen_q=None,
+              max_seqlen_k=None, stream=None) -> AttnVariantDesc:
+    """Build the descriptor for tensors q/k/v/out (see include/attn.h for layouts)."""
+    if q.dtype not in _DTYPES or k.dtype != q.dtype or v.dtype != q.dtype or out.dtype != q.dtype:
+        raise TypeError("q, k, v, out must share dtype bfloat16 or float32")
+    d = AttnVariantDesc.new()
+    d.dtype = _DTYPES[q.dtype]
+    varlen = cu_seqlens_q is not None
+    D = q.shape[-1]
+    d.head_dim = D
+    d.scale = float(scale) if scale is not None else 1.0 / math.sqrt(D)
+    if window is not None:
+        d.mask_kind = ATTN_MASK_SLIDING_WINDOW
+        d.window_left, d.window_right = int(window[0]), int(window[1])
+    else:
+        d.mask_kind = ATTN_MASK_CAUSAL if causal else ATTN_MASK_NONE
+    d.softcap = float(softcap)
+    if alibi_slopes is not None:
+        if alibi_slopes.dtype != torch.float32 or alibi_slopes.device != q.device:
+            raise TypeError("alibi_slopes must be fp32 on q's device")
+        d.alibi_slopes = alibi_slopes.data_ptr()
+    if varlen:
+        if cu_seqlens_k is None:
+            cu_seqlens_k = cu_seqlens_q
+        for cu in (cu_seqlens_q, cu_seqlens_k):
+            if cu.dtype != torch.int32 or cu.device != q.device or not cu.is_contiguous():
+                raise TypeError("cu_seqlens must be contiguous int32 on q's device")
+        if max_seqlen_q is None or max_seqlen_k is None:
+            raise ValueError("varlen needs max_seqlen_q and max_seqlen_k (no device readback)")
+        d.batch = cu_seqlens_q.numel() - 1
+        d.num_q_heads, d.num_kv_heads = q.shape[1], k.shape[1]
+        d.cu_seqlens_q, d.cu_seqlens_k = cu_seqlens_q.data_ptr(), cu_seqlens_k.data_ptr()
+        d.max_seqlen_q, d.max_seqlen_k = int(max_seqlen_q), int(max_seqlen_k)
+        d.total_q, d.total_k = q.shape[0], k.shape[0]
+        for name, t in (("q", q), ("k", k), ("v", v), ("o", out)):
+            setattr(d, f"stride_{name}_h", t.stride(1))
+            setattr(d, f"stride_{name}_s", t.stride(0))
+            if t.stride(2) != 1:
+                raise ValueError("head_dim must be the innermost, contiguous axis")
+    else:
+        d.batch, d.num_q_heads, d.seqlen_q = q.shape[0], q.shape[1], q.shape[2]
+        d.num_kv_heads, d.seqlen_k = k.shape[1], k.shape[2]
+        for name, t in (("q", q), ("k", k), ("v", v), ("o", out)):
+            setattr(d, f"stride_{name}_b", t.stride(0))
+            setattr(d, f"stride_{name}_h", t.stride(1))
+            setattr(d, f"stride_{name}_s", t.stride(2))
+            if t.stride(3) != 1:
+                raise ValueError("head_dim must be the innermost, contiguous axis")
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device).cuda_stream
+    d.stream = stream
+    return d
+
+
+def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softcap: float = 0.0,
+        scale: Optional[float] = None, cu_seqlens_q=None, cu_seqlens_k=None, max_seqlen_q=None,
+        max_seqlen_k=None, out=None, lse=None, return_lse: bool = True):
+    """Attention forward on the GPU.
+
+    Fixed length: q [B,Hq,S,D], k/v [B,Hkv,Sk,D] -> out like q, lse [B,Hq,S] fp32.
+    Varlen: q [Tq,Hq,D], k/v [Tk,Hkv,D], cu_seqlens int32 [B+1] -> lse [Hq,Tq].
+    window=(left, right) selects the sliding-window mask (-1 = unbounded).
+    """
+    if not q.is_cuda:
+        raise ValueError("fwd runs on the GPU only; q, k, v must be device tensors")
+    lib = load()
+    varlen = cu_seqlens_q is not None
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and return_lse:
+        shape = (q.shape[1], q.shape[0]) if varlen else (q.shape[0], q.shape[1], q.shape[2])
+        lse = torch.empty(shape, dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.dtype != torch.float32 or not lse.is_contiguous()):
+        raise TypeError("lse must be contiguous fp32")
+    d = make_desc(q, k, v, out, causal=causal, window=window, alibi_slopes=alibi_slopes,
+                  softcap=softcap, scale=scale, cu_seqlens_q=cu_seqlens_q,
+                  cu_seqlens_k=cu_seqlens_k, max_seqlen_q=max_seqlen_q,
+                  max_seqlen_k=max_seqlen_k)
+    status = lib.attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                          lse.data_ptr() if lse is not None else None, ctypes.byref(d))
+    check(status, lib)
+    return (out, lse) if return_lse else out

@@ -1,0 +1,208 @@
+// attn_api.cpp -- C ABI of libattn.so: validation, planning and dispatch.
+//
+// Every check runs on the host before the first HIP call, so a rejected call
+// has no side effect and the error paths are testable without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+
+#include "../../include/attn.h"
+#include "kernel_params.h"
+#include "launch.h"
+
+namespace {
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+// Resolve one tensor's strides (0 = contiguous default) and check them.
+// Returns ATTN_OK or an error code.
+int resolve_strides(int varlen, int64_t heads, int64_t seqlen, int64_t d, int64_t elt_align,
+                    int64_t in_b, int64_t in_h, int64_t in_s, int64_t* out_b, int64_t* out_h,
+                    int64_t* out_s)
+{
+    int64_t b, h, s;
+    if (varlen) {
+        // [T, H, D]: token stride H*D, head stride D
+        b = 0;
+        h = in_h ? in_h : d;
+        s = in_s ? in_s : heads * d;
+    } else {
+        // [B, H, S, D]
+        s = in_s ? in_s : d;
+        h = in_h ? in_h : seqlen * d;
+        b = in_b ? in_b : heads * seqlen * d;
+    }
+    if (h < 0 || s < 0 || b < 0) return ATTN_ERR_BAD_SHAPE;
+    if (s < d && seqlen > 1) return ATTN_ERR_BAD_SHAPE;  // rows would overlap
+    if ((h % elt_align) || (s % elt_align) || (b % elt_align)) return ATTN_ERR_ALIGNMENT;
+    *out_b = b;
+    *out_h = h;
+    *out_s = s;
+    return ATTN_OK;
+}
+
+// The kernels address one (sequence, head) slice with 32-bit byte offsets.
+bool slice_fits(int64_t rows, int64_t stride_s, int64_t d, int64_t elt_bytes, int64_t pad_rows)
+{
+    if (rows <= 0) return true;
+    int64_t bytes = ((rows + pad_rows) * stride_s + d) * elt_bytes;
+    return bytes < (int64_t(1) << 31);
+}
+
+}  // namespace
+
+extern "C" int attn_abi_version(void) { return ATTN_ABI_VERSION; }
+
+extern "C" const char* attn_status_string(int status)
+{
+    switch (status) {
+    case ATTN_OK: return "ok";
+    case ATTN_ERR_NULL_PTR: return "a required pointer is NULL";
+    case ATTN_ERR_BAD_SHAPE: return "non-positive or inconsistent sizes or strides";
+    case ATTN_ERR_BAD_VARIANT: return "bad mask kind, window, scale or soft-cap";
+    case ATTN_ERR_ALIGNMENT: return "pointer or stride not 16-byte aligned";
+    case ATTN_ERR_UNSUPPORTED: return "head_dim, dtype or size outside the compiled set";
+    case ATTN_ERR_ABI: return "attn_variant_desc.struct_size does not match the library";
+    case ATTN_ERR_LAUNCH: return "the HIP kernel launch failed";
+    default: return "unknown status";
+    }
+}
+
+static KeyBand band_of(const attn_variant_desc* d)
+{
+    KeyBand b;
+    if (d->mask_kind == ATTN_MASK_CAUSAL) {
+        b.wl = -1;
+        b.wr = 0;
+    } else if (d->mask_kind == ATTN_MASK_SLIDING_WINDOW) {
+        b.wl = d->window_left < 0 ? -1 : d->window_left;
+        b.wr = d->window_right < 0 ? -1 : d->window_right;
+    } else {
+        b.wl = -1;
+        b.wr = -1;
+    }
+    return b;
+}
+
+static int check_variant(const attn_variant_desc* d)
+{
+    if (d->mask_kind < ATTN_MASK_NONE || d->mask_kind > ATTN_MASK_SLIDING_WINDOW)
+        return ATTN_ERR_BAD_VARIANT;
+    if (d->mask_kind == ATTN_MASK_SLIDING_WINDOW && (d->window_left < -1 || d->window_right < -1))
+        return ATTN_ERR_BAD_VARIANT;
+    if (!std::isfinite(d->scale) || !(d->scale > 0.0f)) return ATTN_ERR_BAD_VARIANT;
+    if (!std::isfinite(d->softcap) || d->softcap < 0.0f) return ATTN_ERR_BAD_VARIANT;
+    return ATTN_OK;
+}
+
+extern "C" int attn_plan_tiles(const attn_variant_desc* desc, int32_t q0, int32_t rows,
+                               int32_t lq, int32_t lk, int32_t block_n, int32_t out[4])
+{
+    if (!desc || !out) return ATTN_ERR_NULL_PTR;
+    if (desc->struct_size != sizeof(attn_variant_desc)) return ATTN_ERR_ABI;
+    int rc = check_variant(desc);
+    if (rc != ATTN_OK) return rc;
+    if (block_n <= 0 || lq < 0 || lk < 0 || rows < 0 || q0 < 0) return ATTN_ERR_BAD_SHAPE;
+    TilePlan p = plan_tiles(band_of(desc), q0, rows, lq, lk, block_n);
+    out[0] = p.lo;
+    out[1] = p.full_lo;
+    out[2] = p.full_hi;
+    out[3] = p.hi;
+    return ATTN_OK;
+}
+
+extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
+                        const attn_variant_desc* desc)
+{
+    if (!desc) return ATTN_ERR_NULL_PTR;
+    if (desc->struct_size != sizeof(attn_variant_desc)) return ATTN_ERR_ABI;
+    const attn_variant_desc& d = *desc;
+    if (d.dtype != ATTN_BF16 && d.dtype != ATTN_FP32) return ATTN_ERR_UNSUPPORTED;
+    if (d.head_dim != 64 && d.head_dim != 128) return ATTN_ERR_UNSUPPORTED;
+    if (d.batch < 0 || d.num_q_heads <= 0 || d.num_kv_heads <= 0) return ATTN_ERR_BAD_SHAPE;
+    if (d.num_q_heads % d.num_kv_heads != 0) return ATTN_ERR_BAD_SHAPE;
+    int rc = check_variant(&d);
+    if (rc != ATTN_OK) return rc;
+    const int varlen = d.cu_seqlens_q != nullptr;
+    if (varlen && !d.cu_seqlens_k) return ATTN_ERR_NULL_PTR;
+    if (!varlen && d.cu_seqlens_k) return ATTN_ERR_BAD_SHAPE;
+    int64_t max_q, max_k;
+    if (varlen) {
+        if (d.max_seqlen_q < 0 || d.max_seqlen_k < 0 || d.total_q < 0 || d.total_k < 0)
+            return ATTN_ERR_BAD_SHAPE;
+        if (d.total_q > INT32_MAX || d.total_k > INT32_MAX) return ATTN_ERR_UNSUPPORTED;
+        max_q = d.max_seqlen_q;
+        max_k = d.max_seqlen_k;
+    } else {
+        if (d.seqlen_q < 0 || d.seqlen_k < 0) return ATTN_ERR_BAD_SHAPE;
+        max_q = d.seqlen_q;
+        max_k = d.seqlen_k;
+    }
+    const int64_t elt = d.dtype == ATTN_BF16 ? 2 : 4;
+    const int64_t align = 16 / elt;
+    const int64_t D = d.head_dim;
+    AttnParams p = {};
+    rc = resolve_strides(varlen, d.num_q_heads, max_q, D, align, d.stride_q_b, d.stride_q_h,
+                         d.stride_q_s, &p.sq_b, &p.sq_h, &p.sq_s);
+    if (rc == ATTN_OK)
+        rc = resolve_strides(varlen, d.num_kv_heads, max_k, D, align, d.stride_k_b, d.stride_k_h,
+                             d.stride_k_s, &p.sk_b, &p.sk_h, &p.sk_s);
+    if (rc == ATTN_OK)
+        rc = resolve_strides(varlen, d.num_kv_heads, max_k, D, align, d.stride_v_b, d.stride_v_h,
+                             d.stride_v_s, &p.sv_b, &p.sv_h, &p.sv_s);
+    if (rc == ATTN_OK)
+        rc = resolve_strides(varlen, d.num_q_heads, max_q, D, align, d.stride_o_b, d.stride_o_h,
+                             d.stride_o_s, &p.so_b, &p.so_h, &p.so_s);
+    if (rc != ATTN_OK) return rc;
+    // 32-bit offsets inside one slice, with one tile of padding past the end.
+    if (!slice_fits(max_q, p.sq_s, D, elt, 128) || !slice_fits(max_k, p.sk_s, D, elt, 128) ||
+        !slice_fits(max_k, p.sv_s, D, elt, 128) || !slice_fits(max_q, p.so_s, D, elt, 128))
+        return ATTN_ERR_UNSUPPORTED;
+
+    const int block_m = d.dtype == ATTN_BF16 ? attn::bf16_block_m() : attn::f32_block_m();
+    const int64_t q_tiles = (max_q + block_m - 1) / block_m;
+    const int64_t blocks = q_tiles * d.num_q_heads * (int64_t)d.batch;
+    if (blocks > INT32_MAX) return ATTN_ERR_UNSUPPORTED;
+    if (blocks == 0) return ATTN_OK;  // nothing to compute
+
+    if (!q || !k || !v || !out) return ATTN_ERR_NULL_PTR;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+        return ATTN_ERR_ALIGNMENT;
+    if ((reinterpret_cast<uintptr_t>(lse) & 3u) != 0) return ATTN_ERR_ALIGNMENT;
+
+    p.q = q;
+    p.k = k;
+    p.v = v;
+    p.o = out;
+    p.lse = lse;
+    p.slopes = d.alibi_slopes;
+    p.cu_q = d.cu_seqlens_q;
+    p.cu_k = d.cu_seqlens_k;
+    p.batch = d.batch;
+    p.hq = d.num_q_heads;
+    p.hkv = d.num_kv_heads;
+    p.group = d.num_q_heads / d.num_kv_heads;
+    p.seqlen_q = d.seqlen_q;
+    p.seqlen_k = d.seqlen_k;
+    p.num_q_tiles = (int32_t)q_tiles;
+    p.total_q = varlen ? d.total_q : 0;
+    p.band = band_of(&d);
+    p.scale = d.scale;
+    p.scale_log2 = d.scale * 1.4426950408889634f;
+    p.softcap = d.softcap;
+    p.softcap_pre = d.softcap > 0.0f ? d.scale / d.softcap : 0.0f;
+    p.softcap_post = d.softcap * 1.4426950408889634f;
+    // Keep each kv-head group on one XCD when the groups divide evenly.
+    p.map_mode = ((int64_t)d.batch * d.num_kv_heads) % 8 == 0 ? 1 : 0;
+    if (const char* env = std::getenv("ATTN_MAP_MODE")) {
+        int m = std::atoi(env);
+        if (m == 0 || (m == 1 && p.map_mode == 1)) p.map_mode = m;
+    }
+
+    hipStream_t stream = static_cast<hipStream_t>(d.stream);
+    hipError_t err = d.dtype == ATTN_BF16 ? attn::launch_bf16(p, d.head_dim, stream)
+                                          : attn::launch_f32(p, d.head_dim, stream);
+    return err == hipSuccess ? ATTN_OK : ATTN_ERR_LAUNCH;
+}

@@ -1,0 +1,202 @@
+// attn_fwd_f32.hip -- fused attention forward for fp32 inputs on gfx950.
+//
+// fp32 has no faster matrix path on this chip (the fp32 matrix and vector
+// peaks are equal), so each lane owns one query row and accumulates with
+// fp32 vector FMAs. A workgroup is one 64-lane wavefront covering 64 query
+// rows of one (sequence, query head); key/value tiles of 32 keys are staged
+// through LDS and read as broadcasts. The score modifications, the band mask
+// with loop splitting, and the base-2 online softmax are the same as in the
+// bf16 kernel (Eq. 1 and 2 of Section 2.2, Appendix A).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernel_params.h"
+#include "launch.h"
+#include "score_mods.h"
+
+namespace attn {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int BM = 64;  // query rows per workgroup (one per lane)
+constexpr int BN = 32;  // keys per tile
+constexpr int NT = 64;
+
+template <int D, bool SOFTCAP, bool ALIBI>
+__global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
+{
+    __shared__ __attribute__((aligned(16))) float qs[BM][D + 4];  // padded rows
+    __shared__ __attribute__((aligned(16))) float ks[BN][D];
+    __shared__ __attribute__((aligned(16))) float vs[BN][D];
+
+    const int tid = threadIdx.x;
+    const int nbh = p.batch * p.hq;
+    const int w = blockIdx.x;
+    const int qt = p.num_q_tiles - 1 - w / nbh;
+    const int b = (w % nbh) / p.hq, hq = (w % nbh) % p.hq;
+
+    int lq, lk;
+    int64_t qrow0 = 0, krow0 = 0;
+    if (p.cu_q) {
+        qrow0 = p.cu_q[b];
+        lq = p.cu_q[b + 1] - (int)qrow0;
+        krow0 = p.cu_k[b];
+        lk = p.cu_k[b + 1] - (int)krow0;
+    } else {
+        lq = p.seqlen_q;
+        lk = p.seqlen_k;
+    }
+    const int q0 = qt * BM;
+    if (q0 >= lq) return;
+    const int hkv = hq / p.group;
+    const float* qb = static_cast<const float*>(p.q);
+    const float* kb = static_cast<const float*>(p.k);
+    const float* vb = static_cast<const float*>(p.v);
+    float* ob = static_cast<float*>(p.o);
+    int64_t qoff, koff, voff, ooff;
+    if (p.cu_q) {
+        qoff = qrow0 * p.sq_s + (int64_t)hq * p.sq_h;
+        ooff = qrow0 * p.so_s + (int64_t)hq * p.so_h;
+        koff = krow0 * p.sk_s + (int64_t)hkv * p.sk_h;
+        voff = krow0 * p.sv_s + (int64_t)hkv * p.sv_h;
+    } else {
+        qoff = (int64_t)b * p.sq_b + (int64_t)hq * p.sq_h;
+        ooff = (int64_t)b * p.so_b + (int64_t)hq * p.so_h;
+        koff = (int64_t)b * p.sk_b + (int64_t)hkv * p.sk_h;
+        voff = (int64_t)b * p.sv_b + (int64_t)hkv * p.sv_h;
+    }
+
+    const int qi = q0 + tid;
+    {
+        const float* src = qb + qoff + (int64_t)qi * p.sq_s;
+#pragma unroll
+        for (int c = 0; c < D / 4; ++c) {
+            f32x4 x = {0.f, 0.f, 0.f, 0.f};
+            if (qi < lq) x = *reinterpret_cast<const f32x4*>(src + 4 * c);
+            *reinterpret_cast<f32x4*>(&qs[tid][4 * c]) = x;
+        }
+    }
+    int jlo = 1, jhi = 0;
+    if (qi < lq) band_row(p.band, qi, lq, lk, &jlo, &jhi);
+    const int ip = qi + (lk - lq);
+    float slope_log2 = 0.0f;
+    if constexpr (ALIBI) slope_log2 = p.slopes[hq] * kLog2e;
+    constexpr bool MODS = SOFTCAP || ALIBI;
+
+    const TilePlan gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
+    float o[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) o[d] = 0.0f;
+    float m_run = -__builtin_inff(), l_run = 0.0f;
+
+    for (int kt = gp.lo; kt < gp.hi; ++kt) {
+        const int j0 = kt * BN;
+        __syncthreads();  // previous tile fully consumed
+#pragma unroll
+        for (int i = 0; i < BN * D / 4 / NT; ++i) {
+            int e = i * NT + tid;
+            int r = e / (D / 4), c = e % (D / 4);
+            f32x4 kx = {0.f, 0.f, 0.f, 0.f}, vx = {0.f, 0.f, 0.f, 0.f};
+            if (j0 + r < lk) {
+                kx = *reinterpret_cast<const f32x4*>(kb + koff + (int64_t)(j0 + r) * p.sk_s + 4 * c);
+                vx = *reinterpret_cast<const f32x4*>(vb + voff + (int64_t)(j0 + r) * p.sv_s + 4 * c);
+            }
+            *reinterpret_cast<f32x4*>(&ks[r][4 * c]) = kx;
+            *reinterpret_cast<f32x4*>(&vs[r][4 * c]) = vx;
+        }
+        __syncthreads();
+        if (jlo > jhi || jhi < j0 || jlo > j0 + BN - 1) continue;  // row sees none of the tile
+        const bool full = jlo <= j0 && j0 + BN - 1 <= jhi;
+        float s[BN];
+#pragma unroll
+        for (int j = 0; j < BN; ++j) s[j] = 0.0f;
+#pragma unroll
+        for (int c = 0; c < D / 4; ++c) {
+            f32x4 qx = *reinterpret_cast<const f32x4*>(&qs[tid][4 * c]);
+#pragma unroll
+            for (int j = 0; j < BN; ++j) {
+                f32x4 kx = *reinterpret_cast<const f32x4*>(&ks[j][4 * c]);
+                s[j] = __builtin_fmaf(qx[0], kx[0], s[j]);
+                s[j] = __builtin_fmaf(qx[1], kx[1], s[j]);
+                s[j] = __builtin_fmaf(qx[2], kx[2], s[j]);
+                s[j] = __builtin_fmaf(qx[3], kx[3], s[j]);
+            }
+        }
+        float mx = -__builtin_inff();
+#pragma unroll
+        for (int j = 0; j < BN; ++j) {
+            float x = MODS ? score_log2<SOFTCAP, ALIBI>(s[j], p.scale_log2, p.softcap_pre,
+                                                        p.softcap_post, slope_log2, ip, j0 + j)
+                           : s[j] * p.scale_log2;
+            if (!full && (j0 + j < jlo || j0 + j > jhi)) x = -__builtin_inff();
+            s[j] = x;
+            mx = __builtin_fmaxf(mx, x);
+        }
+        const float m_new = __builtin_fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 when m_run = -inf
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int d = 0; d < D; ++d) o[d] *= alpha;
+#pragma unroll
+        for (int j = 0; j < BN; ++j) {
+            float pe = __builtin_amdgcn_exp2f(s[j] - m_new);
+            l_run += pe;
+#pragma unroll
+            for (int c = 0; c < D / 4; ++c) {
+                f32x4 vx = *reinterpret_cast<const f32x4*>(&vs[j][4 * c]);
+                o[4 * c + 0] = __builtin_fmaf(pe, vx[0], o[4 * c + 0]);
+                o[4 * c + 1] = __builtin_fmaf(pe, vx[1], o[4 * c + 1]);
+                o[4 * c + 2] = __builtin_fmaf(pe, vx[2], o[4 * c + 2]);
+                o[4 * c + 3] = __builtin_fmaf(pe, vx[3], o[4 * c + 3]);
+            }
+        }
+    }
+
+    if (qi < lq) {
+        const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+        float* dst = ob + ooff + (int64_t)qi * p.so_s;
+#pragma unroll
+        for (int c = 0; c < D / 4; ++c) {
+            f32x4 x = {o[4 * c] * inv, o[4 * c + 1] * inv, o[4 * c + 2] * inv, o[4 * c + 3] * inv};
+            *reinterpret_cast<f32x4*>(dst + 4 * c) = x;
+        }
+        if (p.lse) {
+            float lse = l_run > 0.0f ? (m_run + __builtin_log2f(l_run)) * kLn2 : -__builtin_inff();
+            int64_t idx = p.cu_q ? (int64_t)hq * p.total_q + qrow0 + qi
+                                 : ((int64_t)b * p.hq + hq) * lq + qi;
+            p.lse[idx] = lse;
+        }
+    }
+}
+
+template <int D, bool SOFTCAP, bool ALIBI>
+hipError_t launch(const AttnParams& p, hipStream_t stream)
+{
+    int64_t blocks = (int64_t)p.num_q_tiles * p.hq * p.batch;
+    hipLaunchKernelGGL((attn_fwd_f32_kernel<D, SOFTCAP, ALIBI>), dim3((unsigned)blocks), dim3(NT),
+                       0, stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int f32_block_m() { return BM; }
+
+hipError_t launch_f32(const AttnParams& p, int head_dim, hipStream_t stream)
+{
+    const bool sc = p.softcap > 0.0f, al = p.slopes != nullptr;
+    if (head_dim == 128) {
+        if (sc && al) return launch<128, true, true>(p, stream);
+        if (sc) return launch<128, true, false>(p, stream);
+        if (al) return launch<128, false, true>(p, stream);
+        return launch<128, false, false>(p, stream);
+    }
+    if (sc && al) return launch<64, true, true>(p, stream);
+    if (sc) return launch<64, true, false>(p, stream);
+    if (al) return launch<64, false, true>(p, stream);
+    return launch<64, false, false>(p, stream);
+}
+
+}  // namespace attn

@@ -1,0 +1,18 @@
+// launch.h -- host-side entry points of the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "kernel_params.h"
+
+namespace attn {
+
+// bf16 inputs, fp32 accumulation; head_dim 64 or 128.
+hipError_t launch_bf16(const AttnParams& p, int head_dim, hipStream_t stream);
+int bf16_block_m();
+
+// fp32 inputs and arithmetic; head_dim 64 or 128.
+hipError_t launch_f32(const AttnParams& p, int head_dim, hipStream_t stream);
+int f32_block_m();
+
+}  // namespace attn

@@ -1,0 +1,133 @@
+"""Helpers shared by the GPU tests: run the HIP path through the C ABI on
+seeded inputs and compare with the CPU oracle element by element."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2605_05023_amd as attn
+from paper_2605_05023_amd.workloads import Inputs
+
+# Tolerances on the output O (max abs error) by dtype, and on LSE.
+O_TOL = {"bf16": 2e-2, "fp32": 1e-4}
+LSE_TOL = 1e-3
+
+
+def gpu_available() -> bool:
+    return torch.cuda.is_available()
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(inp: Inputs, *, out=None, lse=None, q=None, k=None, v=None):
+    """Run the library on `inp` (tensors moved to cuda:0 unless given)."""
+    wl = inp.wl
+    dev = torch.device("cuda:0")
+    q = inp.q.to(dev) if q is None else q
+    k = inp.k.to(dev) if k is None else k
+    v = inp.v.to(dev) if v is None else v
+    slopes = inp.slopes.to(dev) if inp.slopes is not None else None
+    kw = {}
+    if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW:
+        kw["window"] = (wl.window_left, wl.window_right)
+    else:
+        kw["causal"] = wl.mask == attn.ATTN_MASK_CAUSAL
+    if inp.cu_seqlens is not None:
+        cu = inp.cu_seqlens.to(dev)
+        kw.update(cu_seqlens_q=cu, cu_seqlens_k=cu, max_seqlen_q=inp.max_seqlen,
+                  max_seqlen_k=inp.max_seqlen)
+    return attn.fwd(q, k, v, alibi_slopes=slopes, softcap=wl.softcap, scale=wl.scale,
+                    out=out, lse=lse, **kw)
+
+
+def rows_to_index(inp: Inputs, rows):
+    """Flat LSE row ids -> index tuples into O."""
+    rows = np.asarray(rows, dtype=np.int64)
+    if inp.cu_seqlens is not None:
+        T = inp.total_tokens
+        return rows % T, rows // T          # (token, head)
+    B, H, S, _ = inp.q.shape
+    return rows // (H * S), (rows // S) % H, rows % S
+
+
+def compare(inp: Inputs, o_gpu, lse_gpu, rows=None, *, o_tol=None, lse_tol=LSE_TOL, ref=None):
+    """Max abs errors of O and LSE against the oracle on `rows` (all rows if None)."""
+    o_ref, lse_ref = ref if ref is not None else oracle.attention_inputs(inp, rows=rows)
+    o_tol = O_TOL[inp.wl.dtype] if o_tol is None else o_tol
+    if rows is None:
+        og = o_gpu.float().cpu().numpy().astype(np.float64)
+        lg = lse_gpu.cpu().numpy().astype(np.float64)
+        orf, lrf = o_ref, lse_ref
+    else:
+        idx = rows_to_index(inp, rows)
+        tidx = tuple(torch.as_tensor(i, device=o_gpu.device) for i in idx)
+        og = o_gpu[tidx].float().cpu().numpy().astype(np.float64)
+        lg = lse_gpu.reshape(-1)[torch.as_tensor(rows, device=lse_gpu.device)].cpu().numpy()
+        lg = lg.astype(np.float64)
+        orf = o_ref[idx]
+        lrf = lse_ref.reshape(-1)[rows]
+    assert np.isfinite(og).all(), "non-finite values in O"
+    o_err = float(np.max(np.abs(og - orf))) if og.size else 0.0
+    inf_ref = np.isinf(lrf)
+    assert np.array_equal(np.isinf(lg), inf_ref), "LSE -inf pattern differs"
+    assert (lg[inf_ref] == lrf[inf_ref]).all()
+    fin = ~inf_ref
+    lse_err = float(np.max(np.abs(lg[fin] - lrf[fin]))) if fin.any() else 0.0
+    return o_err, lse_err, o_tol, lse_tol
+
+
+def assert_parity(inp, o_gpu, lse_gpu, rows=None, label="", **kw):
+    o_err, lse_err, o_tol, lse_tol = compare(inp, o_gpu, lse_gpu, rows, **kw)
+    log(f"  {label}: max|dO| = {o_err:.3e} (tol {o_tol:.0e}), max|dLSE| = {lse_err:.3e} "
+        f"(tol {lse_tol:.0e})")
+    assert o_err <= o_tol, f"{label}: O error {o_err} > {o_tol}"
+    assert lse_err <= lse_tol, f"{label}: LSE error {lse_err} > {lse_tol}"
+    return o_err, lse_err
+
+
+def sample_rows(inp: Inputs, n_random: int, seed: int = 0, block_m: int = 128):
+    """Flat LSE row ids: n_random seeded random rows plus structural ones (first
+    and last rows of every sequence and head, tile edges of the first/last
+    query tile, window edges)."""
+    rng = np.random.default_rng(seed)
+    wl = inp.wl
+    H = wl.hq
+    rows = set()
+    if inp.cu_seqlens is not None:
+        T = inp.total_tokens
+        total = H * T
+        cu = inp.cu_seqlens.tolist()
+        for h in {0, H // 2, H - 1}:
+            for s in range(len(cu) - 1):
+                a, b = cu[s], cu[s + 1]
+                for t in {a, a + 1, b - 1, b - 2, a + block_m - 1, a + block_m}:
+                    if a <= t < b:
+                        rows.add(h * T + t)
+    else:
+        B, S = inp.q.shape[0], inp.q.shape[2]
+        total = B * H * S
+        for b in {0, B - 1}:
+            for h in {0, H // 2, H - 1}:
+                base = (b * H + h) * S
+                cand = {0, 1, block_m - 1, block_m, S - block_m, S - 1, S - 2}
+                if wl.window_left >= 0:
+                    cand |= {wl.window_left - 1, wl.window_left, wl.window_left + 1,
+                             S // 2 + wl.window_left}
+                for i in cand:
+                    if 0 <= i < S:
+                        rows.add(base + i)
+    rows |= set(rng.choice(total, size=min(n_random, total), replace=False).tolist())
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+def nan_fill_(t):
+    if t.dtype.is_floating_point:
+        t.fill_(math.nan)
+    return t

@@ -1,0 +1,168 @@
+"""The C ABI of libattn.so on the CPU: symbols, versions and every validation
+error path. Validation runs before any HIP call, so none of these calls
+touches a GPU (pointers are dummies that are never dereferenced)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2605_05023_amd as attn
+from paper_2605_05023_amd import _abi
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "attn.h")
+P = 0x10000  # dummy 16-byte aligned device pointers, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return attn.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(attn_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(_abi.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_ctypes_mirror_matches_header(tmp_path):
+    """Compile the header with gcc and compare sizeof and every field offset."""
+    fields = [f[0] for f in _abi.AttnVariantDesc._fields_]
+    src = tmp_path / "layout.c"
+    lines = ["#include <stdio.h>", "#include <stddef.h>", f'#include "{HEADER}"', "int main(void) {",
+             '  printf("%zu\\n", sizeof(attn_variant_desc));']
+    lines += [f'  printf("%zu\\n", offsetof(attn_variant_desc, {f}));' for f in fields]
+    lines += ["  return 0;", "}"]
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", str(src), "-o", str(exe)], check=True)
+    out = [int(x) for x in subprocess.run([str(exe)], check=True, capture_output=True,
+                                          text=True).stdout.split()]
+    assert out[0] == ctypes.sizeof(_abi.AttnVariantDesc)
+    for f, off in zip(fields, out[1:]):
+        assert getattr(_abi.AttnVariantDesc, f).offset == off, f
+
+
+def test_versions_and_strings(lib):
+    assert lib.attn_abi_version() == _abi.ATTN_ABI_VERSION
+    for code in _abi.STATUS:
+        s = lib.attn_status_string(code)
+        assert s and s != b"unknown status"
+    assert lib.attn_status_string(-99) == b"unknown status"
+
+
+def base_desc(varlen=False):
+    d = _abi.AttnVariantDesc.new()
+    d.dtype = _abi.ATTN_BF16
+    d.batch, d.num_q_heads, d.num_kv_heads = 2, 8, 2
+    d.head_dim = 128
+    d.scale = 0.125
+    d.mask_kind = _abi.ATTN_MASK_CAUSAL
+    if varlen:
+        d.cu_seqlens_q = d.cu_seqlens_k = P
+        d.max_seqlen_q = d.max_seqlen_k = 100
+        d.total_q = d.total_k = 150
+    else:
+        d.seqlen_q = d.seqlen_k = 100
+    return d
+
+
+def call(lib, d, q=P, k=P, v=P, o=P, lse=P):
+    return lib.attn_fwd(q, k, v, o, lse, ctypes.byref(d) if d is not None else None)
+
+
+def err(name):
+    return _abi.STATUS_CODE[name]
+
+
+CASES = [
+    ("struct_size", lambda d: setattr(d, "struct_size", 8), "ATTN_ERR_ABI"),
+    ("dtype", lambda d: setattr(d, "dtype", 7), "ATTN_ERR_UNSUPPORTED"),
+    ("head_dim 96", lambda d: setattr(d, "head_dim", 96), "ATTN_ERR_UNSUPPORTED"),
+    ("head_dim 0", lambda d: setattr(d, "head_dim", 0), "ATTN_ERR_UNSUPPORTED"),
+    ("gqa ratio", lambda d: setattr(d, "num_kv_heads", 3), "ATTN_ERR_BAD_SHAPE"),
+    ("zero q heads", lambda d: setattr(d, "num_q_heads", 0), "ATTN_ERR_BAD_SHAPE"),
+    ("zero kv heads", lambda d: setattr(d, "num_kv_heads", 0), "ATTN_ERR_BAD_SHAPE"),
+    ("negative batch", lambda d: setattr(d, "batch", -1), "ATTN_ERR_BAD_SHAPE"),
+    ("negative seqlen", lambda d: setattr(d, "seqlen_q", -5), "ATTN_ERR_BAD_SHAPE"),
+    ("mask kind", lambda d: setattr(d, "mask_kind", 9), "ATTN_ERR_BAD_VARIANT"),
+    ("window < -1", lambda d: (setattr(d, "mask_kind", 2), setattr(d, "window_left", -2)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("window right < -1", lambda d: (setattr(d, "mask_kind", 2), setattr(d, "window_right", -7)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("softcap < 0", lambda d: setattr(d, "softcap", -1.0), "ATTN_ERR_BAD_VARIANT"),
+    ("softcap nan", lambda d: setattr(d, "softcap", float("nan")), "ATTN_ERR_BAD_VARIANT"),
+    ("scale 0", lambda d: setattr(d, "scale", 0.0), "ATTN_ERR_BAD_VARIANT"),
+    ("scale < 0", lambda d: setattr(d, "scale", -0.1), "ATTN_ERR_BAD_VARIANT"),
+    ("scale inf", lambda d: setattr(d, "scale", float("inf")), "ATTN_ERR_BAD_VARIANT"),
+    ("stride not 16B", lambda d: setattr(d, "stride_q_s", 132), "ATTN_ERR_ALIGNMENT"),
+    ("head stride not 16B", lambda d: setattr(d, "stride_k_h", 100 * 128 + 4), "ATTN_ERR_ALIGNMENT"),
+    ("rows overlap", lambda d: setattr(d, "stride_v_s", 64), "ATTN_ERR_BAD_SHAPE"),
+    ("negative stride", lambda d: setattr(d, "stride_o_h", -128), "ATTN_ERR_BAD_SHAPE"),
+    ("slice beyond 2 GiB", lambda d: (setattr(d, "seqlen_k", 1 << 20), setattr(d, "stride_k_s", 1 << 12)),
+     "ATTN_ERR_UNSUPPORTED"),
+    ("cu_k without cu_q", lambda d: setattr(d, "cu_seqlens_k", P), "ATTN_ERR_BAD_SHAPE"),
+]
+
+
+@pytest.mark.parametrize("name,mutate,expect", CASES, ids=[c[0] for c in CASES])
+def test_validation_errors(lib, name, mutate, expect):
+    d = base_desc()
+    mutate(d)
+    assert call(lib, d) == err(expect)
+
+
+VARLEN_CASES = [
+    ("cu_k missing", lambda d: setattr(d, "cu_seqlens_k", None), "ATTN_ERR_NULL_PTR"),
+    ("max_seqlen < 0", lambda d: setattr(d, "max_seqlen_q", -1), "ATTN_ERR_BAD_SHAPE"),
+    ("total < 0", lambda d: setattr(d, "total_k", -1), "ATTN_ERR_BAD_SHAPE"),
+    ("total beyond int32", lambda d: setattr(d, "total_q", 1 << 33), "ATTN_ERR_UNSUPPORTED"),
+]
+
+
+@pytest.mark.parametrize("name,mutate,expect", VARLEN_CASES, ids=[c[0] for c in VARLEN_CASES])
+def test_varlen_validation_errors(lib, name, mutate, expect):
+    d = base_desc(varlen=True)
+    mutate(d)
+    assert call(lib, d) == err(expect)
+
+
+def test_pointer_errors(lib):
+    assert call(lib, None) == err("ATTN_ERR_NULL_PTR")
+    d = base_desc()
+    for kw in ({"q": None}, {"k": None}, {"v": None}, {"o": None}):
+        assert call(lib, d, **kw) == err("ATTN_ERR_NULL_PTR")
+    for kw in ({"q": P + 2}, {"k": P + 8}, {"v": P + 4}, {"o": P + 1}):
+        assert call(lib, d, **kw) == err("ATTN_ERR_ALIGNMENT")
+    assert call(lib, d, lse=P + 2) == err("ATTN_ERR_ALIGNMENT")
+
+
+def test_fp32_alignment_unit(lib):
+    d = base_desc()
+    d.dtype = _abi.ATTN_FP32
+    d.stride_q_s = 132  # 4-element multiple: fine for fp32 ...
+    d.stride_q_h = 132 * 100
+    d.stride_q_b = 132 * 100 * 8
+    d.seqlen_q = 0       # ... and an empty problem returns before any launch
+    assert call(lib, d) == 0
+    d.stride_q_s = 130   # not a multiple of 4 fp32 elements
+    assert call(lib, d) == err("ATTN_ERR_ALIGNMENT")
+
+
+def test_empty_problems_do_nothing(lib):
+    for mut in (lambda d: setattr(d, "batch", 0), lambda d: setattr(d, "seqlen_q", 0)):
+        d = base_desc()
+        mut(d)
+        assert call(lib, d, q=None, k=None, v=None, o=None, lse=None) == 0
+    d = base_desc(varlen=True)
+    d.max_seqlen_q = 0
+    assert call(lib, d, q=None, k=None, v=None, o=None, lse=None) == 0
