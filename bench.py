@@ -1,0 +1,289 @@
+"""Benchmark of the fused attention forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload causal_bf16]
+
+A step is one attn_fwd call (the whole fused forward) over one batch of the
+seeded synthetic workload, with inputs already resident in HBM. Prints one
+JSON line: throughput in TFLOP/s counting only unmasked score entries
+(4 * head_dim FLOPs per visible query/key pair per query head), the roofline
+of the kernel against the bf16 matrix-core peak, and the CPU oracle timed on a
+bounded sample of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2605_05023_amd as attn  # noqa: E402
+from paper_2605_05023_amd.workloads import WORKLOADS, make_inputs  # noqa: E402
+
+METRIC = "attention fwd TFLOP/s (unmasked FLOPs) and % of bf16 MFMA peak, 1 MI355X"
+# Dense bf16 matrix-core peak: 256 CUs x 2.4 GHz x 4096 FLOP/clk/CU (the published 2.5 PFLOP/s).
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_FP32_TFLOPS = 157.3
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2605_05023_amd/csrc/attn_fwd_bf16.hip",
+                  "paper_2605_05023_amd/csrc/attn_fwd_f32.hip",
+                  "paper_2605_05023_amd/csrc/score_mods.h",
+                  "paper_2605_05023_amd/csrc/plan.h",
+                  "paper_2605_05023_amd/csrc/kernel_params.h"]
+MASK_NAMES = {0: "none", 1: "causal", 2: "sliding_window"}
+
+
+def visible_pairs(inp) -> int:
+    """Visible (query, key) pairs summed over query heads, in closed form per row:
+    row i sees keys max(0, i - wl) .. min(S - 1, i + wr) of its own sequence."""
+    wl = inp.wl
+    lengths = inp.lengths if inp.lengths is not None else [wl.seqlen] * wl.batch
+    left = wl.window_left if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW else -1
+    if wl.mask == attn.ATTN_MASK_CAUSAL:
+        right = 0
+    elif wl.mask == attn.ATTN_MASK_SLIDING_WINDOW:
+        right = wl.window_right
+    else:
+        right = -1
+    total = 0
+    for S in lengths:
+        i = np.arange(S, dtype=np.int64)
+        lo = np.zeros(S, np.int64) if left < 0 else np.maximum(0, i - left)
+        hi = np.full(S, S - 1, np.int64) if right < 0 else np.minimum(S - 1, i + right)
+        total += int(np.maximum(0, hi - lo + 1).sum())
+    return total * wl.hq
+
+
+def algorithmic_bytes(inp) -> int:
+    """Bytes the method must move once: Q, K, V in; O and fp32 LSE out."""
+    el = inp.q.element_size()
+    return (2 * inp.q.numel() + inp.k.numel() + inp.v.numel()) * el + \
+        (inp.q.numel() // inp.wl.head_dim) * 4
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload: str):
+    """HBM bytes per launch from the committed PMC summary, if it was measured on
+    the current kernel sources (else None)."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"kernel_hash:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(inp, flops_per_row_fn, min_seconds: float, max_seconds: float, seed: int):
+    """Time the CPU oracle (as it stands) on a seeded random sample of rows."""
+    import oracle  # the benchmark's CPU-baseline leg is allowed to run the oracle
+
+    wl = inp.wl
+    qn = inp.q.float().numpy()
+    kn = inp.k.float().numpy()
+    vn = inp.v.float().numpy()
+    total_rows = qn.shape[0] * qn.shape[1] if inp.cu_seqlens is not None else \
+        qn.shape[0] * qn.shape[1] * qn.shape[2]
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(total_rows)
+    kw = dict(scale=wl.scale, mask=wl.mask, window_left=wl.window_left,
+              window_right=wl.window_right, slopes=inp.slopes, softcap=wl.softcap,
+              cu_seqlens_q=inp.cu_seqlens, cu_seqlens_k=inp.cu_seqlens)
+    oracle.load()
+    done, elapsed, flops, batch = 0, 0.0, 0, 256
+    while done < total_rows and elapsed < min_seconds:
+        rows = order[done:done + batch]
+        t0 = time.perf_counter()
+        oracle.attention(qn, kn, vn, rows=rows, **kw)
+        dt = time.perf_counter() - t0
+        elapsed += dt
+        flops += flops_per_row_fn(rows)
+        done += len(rows)
+        if elapsed + 2 * dt > max_seconds:
+            break
+        batch = min(batch * 2, 16384)
+    return {
+        "value": flops / elapsed / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"{done} of {total_rows} query rows (seeded random), fp64 dense "
+                  f"materialised scores, {elapsed:.1f} s; unit counts unmasked FLOPs of the "
+                  f"sampled rows",
+    }
+
+
+def row_flops_fn(inp):
+    """Unmasked FLOPs of given flat LSE row ids."""
+    wl = inp.wl
+    D = wl.head_dim
+    left = wl.window_left if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW else -1
+    right = 0 if wl.mask == attn.ATTN_MASK_CAUSAL else (
+        wl.window_right if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW else -1)
+    if inp.cu_seqlens is not None:
+        cu = inp.cu_seqlens.numpy().astype(np.int64)
+        T = inp.total_tokens
+
+        def pos(rows):
+            t = rows % T
+            s = np.searchsorted(cu, t, side="right") - 1
+            return t - cu[s], cu[s + 1] - cu[s]
+    else:
+        S = wl.seqlen
+
+        def pos(rows):
+            return rows % S, np.full(len(rows), S)
+
+    def fn(rows):
+        i, L = pos(np.asarray(rows, dtype=np.int64))
+        lo = np.zeros_like(i) if left < 0 else np.maximum(0, i - left)
+        hi = L - 1 if right < 0 else np.minimum(L - 1, i + right)
+        return int(4 * D * np.maximum(0, hi - lo + 1).sum())
+    return fn
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="causal_bf16", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="minimum oracle time for the CPU baseline sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one 1 GiB device copy (counter calibration under rocprofv3)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one MI355X "
+              f"(the kernel on one GPU's share); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+
+    dev = torch.device("cuda:0")
+    wl = WORKLOADS[args.workload]
+    inp = make_inputs(wl)
+    q, k, v = inp.q.to(dev), inp.k.to(dev), inp.v.to(dev)
+    out = torch.empty_like(q)
+    varlen = inp.cu_seqlens is not None
+    lse_shape = (wl.hq, inp.total_tokens) if varlen else (wl.batch, wl.hq, wl.seqlen)
+    lse = torch.empty(lse_shape, dtype=torch.float32, device=dev)
+    slopes = inp.slopes.to(dev) if inp.slopes is not None else None
+    cu = inp.cu_seqlens.to(dev) if varlen else None
+    kw = {}
+    if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW:
+        kw["window"] = (wl.window_left, wl.window_right)
+    else:
+        kw["causal"] = wl.mask == attn.ATTN_MASK_CAUSAL
+    if varlen:
+        kw.update(cu_seqlens_q=cu, cu_seqlens_k=cu, max_seqlen_q=inp.max_seqlen,
+                  max_seqlen_k=inp.max_seqlen)
+    stream = torch.cuda.current_stream(dev)
+    desc = attn.make_desc(q, k, v, out, alibi_slopes=slopes, softcap=wl.softcap, scale=wl.scale,
+                          stream=stream.cuda_stream, **kw)
+    lib = attn.load()
+    args_c = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+              ctypes.byref(desc))
+
+    def step():
+        rc = lib.attn_fwd(*args_c)
+        if rc != 0:
+            attn.check(rc, lib)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = e0.elapsed_time(e1) / args.steps
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    flops = 4 * wl.head_dim * visible_pairs(inp)
+    ms_per_step = wall * 1e3 / args.steps
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    achieved = flops / (kernel_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    traffic = read_traffic(args.workload)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0, sigma^2) inputs; no dataset)",
+        "config": {
+            "workload": args.workload,
+            "batch": wl.batch,
+            "heads_q": wl.hq,
+            "heads_kv": wl.hkv,
+            "seqlen": wl.seqlen if not varlen else f"varlen, total {inp.total_tokens}",
+            "head_dim": wl.head_dim,
+            "mask": MASK_NAMES[wl.mask],
+            "window": [wl.window_left, wl.window_right] if wl.mask == 2 else None,
+            "alibi": wl.alibi,
+            "softcap": wl.softcap,
+            "unmasked_flops_per_step": flops,
+        },
+        "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": traffic,
+            "kernel_avg_ms": round(kernel_ms, 5),
+            "algorithmic_bytes": algorithmic_bytes(inp),
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(inp, row_flops_fn(inp), args.cpu_seconds,
+                                              4 * args.cpu_seconds, seed=wl.seed)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
