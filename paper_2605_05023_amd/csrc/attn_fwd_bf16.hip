@@ -1,32 +1,42 @@
 // attn_fwd_bf16.hip -- fused attention forward for bf16 inputs on gfx950.
 //
 // One workgroup computes BM = 128 query rows of one (sequence, query head):
-// four wavefronts of 32 rows each. It streams the key/value tiles of BN = 64
-// keys that the mask leaves visible through LDS (double-buffered), computes
-// the tile's scores on the bf16 matrix cores with fp32 accumulation, applies
-// the score modifications and, on partial tiles only, the mask in registers,
-// keeps an online softmax per row, and accumulates P V on the matrix cores
-// (Eq. 1 and 2 of Section 2.2; the Score / Mask / Norm stages of Appendix A;
-// loop splitting of Section 3.4 and block skipping of Appendix C).
+// four wavefronts of 32 rows each. It streams the key/value tiles of BN keys
+// (32 or 64) that the mask leaves visible through LDS, computes the scores on the
+// bf16 matrix cores with fp32 accumulation, applies the score modifications
+// and, on partial tiles only, the mask in registers, keeps an online softmax
+// per row, and accumulates P V on the matrix cores (Eq. 1 and 2 of Section
+// 2.2; the Score / Mask / Norm stages of Appendix A; loop splitting of
+// Section 3.4 and block skipping of Appendix C).
 //
 // Layout choices for the 64-wide wavefront and v_mfma_f32_32x32x16_bf16:
 //  * Scores are computed transposed, S^T = K Q^T, so a lane owns one query
 //    row (lane % 32) and 16 keys per 32-key block. The row max and row sum
-//    are then per-lane reductions plus one exchange with lane ^ 32.
+//    are per-lane reductions plus one exchange with lane ^ 32.
 //  * K rows are fed to the A operand in the order pi(r) (bits 2 and 3 of the
-//    row index swapped). With that order the accumulator of lane half h holds
-//    keys 8h..8h+7 and 16+8h..16+8h+7 of the block in registers 0..7 and 8..15,
-//    which is exactly the B-operand layout of the P V product. P never leaves
-//    the registers.
-//  * V is stored transposed in LDS (V^T, keys contiguous) so the A operand of
-//    O^T = V^T P^T is one 16-byte LDS read per lane; the transpose happens in
-//    registers while the tile is staged from global memory.
-//  * O^T rows (head-dim) go through the same pi order, so a lane ends with 8
-//    consecutive head-dim values per half block: 16-byte stores.
-//  * LDS rows use an XOR swizzle of their 16-byte chunks so the A-operand
-//    reads of 8 consecutive lanes hit 8 distinct bank groups.
+//    row index swapped). The accumulator of lane half h then holds keys
+//    8h..8h+7 and 16+8h..16+8h+7 of each 32-key block in registers 0..7 and
+//    8..15: exactly the B-operand layout of the P V product, so P never
+//    leaves the registers.
+//  * K and V tiles go from global memory straight into LDS (buffer loads with
+//    an LDS destination; rows past the sequence end read as zero) in their
+//    natural row-major layout. The A operand of O^T = V^T P^T is assembled by
+//    two LDS transpose reads (ds_read_b64_tr_b16): in each 16-lane group,
+//    output lane 4a+b element f is element b of source lane a+4f, so source
+//    lanes that point at four consecutive head-dim values of four key rows
+//    deliver one head-dim column across four keys to each output lane.
+//  * 16-byte chunks of each LDS row are XOR-swizzled with a function of the
+//    key index chosen so that both the K reads (16 rows, same chunk) and the
+//    transpose reads of V (4 rows x 64 bytes) cover all 64 banks once.
+//  * Software pipeline per iteration j: the QK^T products of tile j+1 are
+//    issued alongside the exponentials of tile j, and the P V products of
+//    tile j alongside the score mods, mask and row max of tile j+1. K tiles
+//    are loaded two tiles ahead and V tiles one tile ahead, so each
+//    iteration needs a single barrier.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <utility>
 
 #include "kernel_params.h"
 #include "launch.h"
@@ -38,17 +48,48 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int BM = 128;    // query rows per workgroup
-constexpr int BN = 64;     // keys per tile
-constexpr int NT = 256;    // threads per workgroup (4 waves)
+constexpr int BM = 128;      // query rows per workgroup
+constexpr int NT = 256;      // threads per workgroup (4 waves)
 constexpr float TAU = 8.0f;  // lazy-rescale threshold, log2 units
+
+// Instruction classes for __builtin_amdgcn_sched_group_barrier.
+constexpr int SG_VALU = 0x2, SG_MFMA = 0x8, SG_DS_READ = 0x100, SG_TRANS = 0x400;
+
+template <int D_, int BN_, bool SOFTCAP_, bool ALIBI_>
+struct Traits {
+    static constexpr int D = D_, BN = BN_;
+    static constexpr bool SOFTCAP = SOFTCAP_, ALIBI = ALIBI_, MODS = SOFTCAP_ || ALIBI_;
+    static constexpr int NB = BN / 32;                   // 32-key blocks per tile
+    static constexpr int ROWB = D * 2;                   // bytes per K/V row in LDS
+    static constexpr int TILE = BN * ROWB;               // bytes per K or V tile
+    static constexpr int LOADS = TILE / (NT * 16);       // 16-byte loads per thread per tile
+    static constexpr int ROWS_PER_LOAD = NT * 16 / ROWB; // tile rows covered by one load round
+    static constexpr int KSTEPS = D / 16;                // MFMA k-steps over the head dim
+    static constexpr int DBLK = D / 32;                  // 32-row blocks of O^T
+    static_assert(BN == 32 || BN == 64, "key tile");
+    static_assert(LOADS >= 1 && LOADS * NT * 16 == TILE, "tile split");
+    static_assert(ROWS_PER_LOAD % 16 == 0, "swizzle period");
+};
 
 // pi: swap bits 2 and 3 of a row index within a 32-row block.
 __device__ __forceinline__ int pi32(int r)
 {
     return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+// XOR applied to the 16-byte chunk index of key row `key` in LDS.
+template <int D>
+__device__ __forceinline__ int chunk_swizzle(int key)
+{
+    if constexpr (D == 128)
+        return ((key & 3) << 2) | ((key >> 2) & 3);
+    else
+        return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes)
@@ -58,100 +99,36 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
                                              0x00020000);
 }
 
-template <int D>
-struct Cfg {
-    static constexpr int CHUNKS = D / 8;                 // 16-byte chunks per K row
-    static constexpr int K_BYTES = BN * D * 2;           // one K tile
-    static constexpr int V_BYTES = D * BN * 2;           // one V^T tile
-    static constexpr int STAGE = K_BYTES + V_BYTES;
-    static constexpr int K_PASSES = BN * CHUNKS / NT;    // 16-byte K loads per thread
-    static constexpr int V_KPT = BN * D / (8 * NT);      // keys per thread in the V transpose
-    static constexpr int V_GROUPS = BN / V_KPT;          // key groups per d-chunk
-    static constexpr int KSTEPS = D / 16;                // MFMA k-steps over the head dim
-    static constexpr int DBLK = D / 32;                  // 32-row blocks of O^T
-    static_assert(K_PASSES * NT == BN * CHUNKS, "K tile split");
-    static_assert(V_GROUPS * (D / 8) == NT, "V tile split");
-};
-
-// Byte offset of chunk c of K row r inside a K tile.
-template <int D>
-__device__ __forceinline__ int k_off(int r, int c)
+// Direct loads: load p of wave w fills the 1 KiB LDS block 4p + w of a tile;
+// lane L writes its bytes 16L..16L+15, which hold (row, chunk) with
+// chunk = physical chunk ^ swizzle(row). Rows of load p are those of load 0
+// plus p * ROWS_PER_LOAD, and the swizzle only sees the row modulo 16, so the
+// per-lane byte offset is the same for every p; the row step goes into the
+// (scalar) buffer descriptor.
+template <class T>
+__device__ __forceinline__ uint32_t load_lane_offset(int wave, int lane, int64_t stride)
 {
-    constexpr int mask = (D / 8) - 1;
-    return r * D * 2 + ((c ^ (pi32(r & 31) & mask)) << 4);
+    int pos = wave * 1024 + 16 * lane;
+    int row = pos / T::ROWB;
+    int pc = (pos % T::ROWB) / 16;
+    int c = pc ^ chunk_swizzle<T::D>(row);
+    return (uint32_t)(((int64_t)row * stride + 8 * c) * 2);
 }
 
-// Byte offset of key byte `kb` (0..127) of V^T row d inside a V^T tile.
-__device__ __forceinline__ int vt_off(int d, int kbyte)
+// Issue the direct global->LDS loads of one tile (rows j0..j0+BN-1 of a slice
+// whose first row is at `base`; rows at or past `rows` read as zero).
+template <class T>
+__device__ __forceinline__ void issue_tile(char* lds_tile, const __bf16* base, int j0, int rows,
+                                           int64_t stride, uint32_t lane_off, int wave)
 {
-    int c = kbyte >> 4;
-    return d * (BN * 2) + (((c ^ (pi32(d & 31) & 7)) << 4) | (kbyte & 15));
-}
-
-template <int D>
-struct TileRegs {
-    u32x4 k[Cfg<D>::K_PASSES];
-    u32x4 v[Cfg<D>::V_KPT];
-};
-
-// Issue the global loads of key tile `kt` (rows j0..j0+BN-1) into registers.
-// Rows at or past the sequence end fall outside the buffer range and read 0.
-template <int D>
-__device__ __forceinline__ void load_tile(TileRegs<D>& r, __amdgpu_buffer_rsrc_t krs,
-                                          __amdgpu_buffer_rsrc_t vrs, int j0, int64_t ks,
-                                          int64_t vs, int tid)
-{
-    using C = Cfg<D>;
 #pragma unroll
-    for (int p = 0; p < C::K_PASSES; ++p) {
-        int ci = p * NT + tid;
-        int row = ci / C::CHUNKS, ch = ci % C::CHUNKS;
-        uint32_t off = (uint32_t)(((int64_t)(j0 + row) * ks + ch * 8) * 2);
-        r.k[p] = __builtin_amdgcn_raw_buffer_load_b128(krs, off, 0, 0);
-    }
-    int kg = tid % C::V_GROUPS, dc = tid / C::V_GROUPS;
-#pragma unroll
-    for (int u = 0; u < C::V_KPT; ++u) {
-        int row = kg * C::V_KPT + u;
-        uint32_t off = (uint32_t)(((int64_t)(j0 + row) * vs + dc * 8) * 2);
-        r.v[u] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off, 0, 0);
-    }
-}
-
-// Write staged registers into one LDS stage: K as rows, V transposed.
-template <int D>
-__device__ __forceinline__ void store_tile(const TileRegs<D>& r, char* stage, int tid)
-{
-    using C = Cfg<D>;
-#pragma unroll
-    for (int p = 0; p < C::K_PASSES; ++p) {
-        int ci = p * NT + tid;
-        int row = ci / C::CHUNKS, ch = ci % C::CHUNKS;
-        *reinterpret_cast<u32x4*>(stage + k_off<D>(row, ch)) = r.k[p];
-    }
-    char* vt = stage + C::K_BYTES;
-    int kg = tid % C::V_GROUPS, dc = tid / C::V_GROUPS;
-    int kbyte = kg * C::V_KPT * 2;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            int d = dc * 8 + 2 * m + e;
-            if constexpr (C::V_KPT == 4) {
-                u32x2 w;
-#pragma unroll
-                for (int q = 0; q < 2; ++q) {
-                    uint32_t a = r.v[2 * q][m], b = r.v[2 * q + 1][m];
-                    w[q] = e == 0 ? ((a & 0xffffu) | (b << 16)) : ((a >> 16) | (b & 0xffff0000u));
-                }
-                *reinterpret_cast<u32x2*>(vt + vt_off(d, kbyte)) = w;
-            } else {
-                static_assert(C::V_KPT == 2, "V transpose width");
-                uint32_t a = r.v[0][m], b = r.v[1][m];
-                uint32_t w = e == 0 ? ((a & 0xffffu) | (b << 16)) : ((a >> 16) | (b & 0xffff0000u));
-                *reinterpret_cast<uint32_t*>(vt + vt_off(d, kbyte)) = w;
-            }
-        }
+    for (int p = 0; p < T::LOADS; ++p) {
+        const int r0 = j0 + p * T::ROWS_PER_LOAD;
+        const int left = rows - r0;
+        const uint32_t bytes = left <= 0 ? 0u : (uint32_t)((((int64_t)left - 1) * stride + T::D) * 2);
+        __amdgpu_buffer_rsrc_t rs = make_rsrc(base + (int64_t)r0 * stride, bytes);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (lds_void*)(lds_tile + (4 * p + wave) * 1024), 16, lane_off, 0, 0, 0);
     }
 }
 
@@ -164,8 +141,48 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b)
     return __builtin_bit_cast(uint32_t, v);
 }
 
+// Lanes l and l ^ 32 hold the two halves of the same query row.
+__device__ __forceinline__ float pair_max(float x)
+{
+    auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
+                                              __builtin_bit_cast(uint32_t, x), false, false);
+    return __builtin_fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]),
+                           __builtin_bit_cast(float, (uint32_t)r[1]));
+}
+
+__device__ __forceinline__ float pair_sum(float x)
+{
+    auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
+                                              __builtin_bit_cast(uint32_t, x), false, false);
+    return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+
 struct WorkItem {
     int b, hq, qt;
+};
+
+// Compile-time loop: f(std::integral_constant<int, i>) for i = 0..N-1, so
+// every index is a constant and per-iteration arrays stay in registers.
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f)
+{
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int V>
+struct Parity {
+    static constexpr int value = V;
+};
+
+template <bool V>
+struct Bool {
+    static constexpr bool value = V;
 };
 
 // Map the hardware workgroup id to (sequence, query head, query tile).
@@ -196,104 +213,251 @@ __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
     return it;
 }
 
-// One key tile for one wavefront: S^T = K Q^T on the matrix cores, score
-// mods, the element mask when MASKED (partial tiles only), online softmax with
-// lazy rescaling, then O^T += V^T P^T.
-template <int D, bool SOFTCAP, bool ALIBI, bool MASKED>
-__device__ __forceinline__ void tile_step(const char* st, const bf16x8 (&qf)[Cfg<D>::KSTEPS],
-                                          f32x16 (&oacc)[Cfg<D>::DBLK], float& m_run, float& l_run,
-                                          const AttnParams& p, int j0, int li, int lh, int jlo,
-                                          int jhi, int ip, float slope_log2)
+// Per-wavefront state carried through the key loop.
+template <class T>
+struct WaveState {
+    bf16x8 qf[T::KSTEPS];      // Q fragment (B operand of S^T)
+    int kaddr[T::KSTEPS];      // LDS byte offsets of this lane's K reads
+    int vaddr[T::DBLK][2];     // LDS byte offsets of this lane's V transpose reads
+    f32x16 oacc[T::DBLK];      // O^T accumulator
+    f32x16 s[T::NB];           // scores of the current tile
+    float m_run, l_run, alpha;
+    bool need;
+    // row constants
+    int lh, jlo, jhi, ip;
+    float slope_log2;
+};
+
+// S^T = K Q^T for the K tile in LDS at `kt`.
+template <class T>
+__device__ __forceinline__ void qk_tile(const char* kt, const WaveState<T>& ws, f32x16 (&s)[T::NB])
 {
-    using C = Cfg<D>;
-    f32x16 sacc[2];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int t = 0; t < T::KSTEPS; ++t) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[b][e] = 0.0f;
-#pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t) {
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            int r = 32 * b + pi32(li);
-            bf16x8 a = *reinterpret_cast<const bf16x8*>(st + k_off<D>(r, 2 * t + lh));
-            sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[t], sacc[b], 0, 0, 0);
+        for (int b = 0; b < T::NB; ++b) {
+            bf16x8 a = *reinterpret_cast<const bf16x8*>(kt + 32 * b * T::ROWB + ws.kaddr[t]);
+            s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ws.qf[t], t == 0 ? f32x16{} : s[b], 0,
+                                                           0, 0);
         }
     }
-    // Element (b, e) is key j0 + 32b + 8lh + e + (e >= 8 ? 8 : 0).
-    constexpr bool MODS = SOFTCAP || ALIBI;
+}
+
+// Score mods, element mask (MASKED) and the tile's row max, in log2 units.
+template <class T, bool MASKED>
+__device__ __forceinline__ float mods_and_max(f32x16 (&s)[T::NB], const AttnParams& p,
+                                              const WaveState<T>& ws, int j0)
+{
     float mx = -__builtin_inff();
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            int j = j0 + 32 * b + 8 * lh + e + (e >= 8 ? 8 : 0);
-            float x = sacc[b][e];
-            if constexpr (MODS)
-                x = score_log2<SOFTCAP, ALIBI>(x, p.scale_log2, p.softcap_pre, p.softcap_post,
-                                               slope_log2, ip, j);
+            // element (b, e) is key j0 + 32b + 8lh + e + (e >= 8 ? 8 : 0)
+            int j = j0 + 32 * b + 8 * ws.lh + e + (e >= 8 ? 8 : 0);
+            float x = s[b][e];
+            if constexpr (T::MODS)
+                x = score_log2<T::SOFTCAP, T::ALIBI>(x, p.scale_log2, p.softcap_pre,
+                                                     p.softcap_post, ws.slope_log2, ws.ip, j);
             if constexpr (MASKED)
-                if (j < jlo || j > jhi) x = -__builtin_inff();
-            sacc[b][e] = x;
+                if (j < ws.jlo || j > ws.jhi) x = -__builtin_inff();
+            s[b][e] = x;
             mx = __builtin_fmaxf(mx, x);
         }
     }
-    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32));
-    if constexpr (!MODS) mx *= p.scale_log2;  // raw max -> log2 units (scale > 0)
-    const float m_new = __builtin_fmaxf(m_run, mx);
-    const bool need = m_new > m_run + TAU;
-    if (__builtin_amdgcn_ballot_w64(need)) {
-        float alpha = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-        if (need) m_run = m_new;
-        l_run *= alpha;
+    mx = pair_max(mx);
+    if constexpr (!T::MODS) mx *= p.scale_log2;  // raw max -> log2 units (scale > 0)
+    return mx;
+}
+
+// Fold a tile max into the running max; decide whether O must be rescaled
+// (only when the max grew by more than TAU, so exp2 arguments stay <= TAU).
+template <class T>
+__device__ __forceinline__ void update_max(WaveState<T>& ws, float mx)
+{
+    const float m_new = __builtin_fmaxf(ws.m_run, mx);
+    ws.need = m_new > ws.m_run + TAU;
+    ws.alpha = ws.need ? __builtin_amdgcn_exp2f(ws.m_run - m_new) : 1.0f;
+    if (ws.need) ws.m_run = m_new;
+}
+
+template <class T>
+__device__ __forceinline__ void rescale_if_needed(WaveState<T>& ws)
+{
+    if (__builtin_amdgcn_ballot_w64(ws.need)) {
+        ws.l_run *= ws.alpha;
 #pragma unroll
-        for (int d = 0; d < C::DBLK; ++d)
+        for (int d = 0; d < T::DBLK; ++d)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) oacc[d][e] *= alpha;
+            for (int e = 0; e < 16; ++e) ws.oacc[d][e] *= ws.alpha;
     }
-    const float m_use = m_run == -__builtin_inff() ? 0.0f : m_run;
+}
+
+// P = exp2(S - m) as bf16 B operands of the P V product, plus the row sum.
+template <class T>
+__device__ __forceinline__ void exp_tile(f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2], float m_use,
+                                         float scale_log2, float& l_run)
+{
     float rs = 0.0f;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            float x = sacc[b][e];
-            float y = MODS ? x - m_use : __builtin_fmaf(x, p.scale_log2, -m_use);
-            float pe = __builtin_amdgcn_exp2f(y);
-            sacc[b][e] = pe;
-            rs += pe;
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                float x0 = s[b][8 * u + 2 * q], x1 = s[b][8 * u + 2 * q + 1];
+                float y0 = T::MODS ? x0 - m_use : __builtin_fmaf(x0, scale_log2, -m_use);
+                float y1 = T::MODS ? x1 - m_use : __builtin_fmaf(x1, scale_log2, -m_use);
+                float p0 = __builtin_amdgcn_exp2f(y0), p1 = __builtin_amdgcn_exp2f(y1);
+                rs += p0;
+                rs += p1;
+                pw[b][u][q] = pack_bf16(p0, p1);
+            }
         }
     }
     l_run += rs;
-    // O^T += V^T P^T over four 16-key steps.
+}
+
+// O^T += V^T P^T for the V tile in LDS at `vt`.
+template <class T>
+__device__ __forceinline__ void pv_tile(const char* vt, const u32x4 (&pw)[T::NB][2], WaveState<T>& ws)
+{
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            u32x4 pw;
+            bf16x8 pb = __builtin_bit_cast(bf16x8, pw[b][u]);
+            const int kb = (32 * b + 16 * u) * T::ROWB;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                pw[q] = pack_bf16(sacc[b][8 * u + 2 * q], sacc[b][8 * u + 2 * q + 1]);
-            bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-            int kbyte = (32 * b + 16 * u + 8 * lh) * 2;
-#pragma unroll
-            for (int d = 0; d < C::DBLK; ++d) {
-                int dr = 32 * d + pi32(li);
-                bf16x8 a = *reinterpret_cast<const bf16x8*>(st + C::K_BYTES + vt_off(dr, kbyte));
-                oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[d], 0, 0, 0);
+            for (int d = 0; d < T::DBLK; ++d) {
+                s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4*)(vt + kb + ws.vaddr[d][0]));
+                s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4*)(vt + kb + ws.vaddr[d][1]));
+                s16x8 a8 = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                ws.oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, a8), pb, ws.oacc[d], 0, 0, 0);
             }
         }
     }
 }
 
-template <int D, bool SOFTCAP, bool ALIBI>
+// One pipelined step, written out as explicit slices. Each QK^T slice issues
+// one MFMA of S_next = Q K_next^T, the K read of the MFMA PF slices later and
+// an equal share of the exponentials of the current tile (P and row sum);
+// each P V slice issues one MFMA of O^T += V^T P^T, the two transpose reads
+// of a later MFMA and a share of the score mods, mask and max of S_next. A
+// scheduling barrier after every slice keeps this order, so the vector work
+// runs while the matrix cores are busy and LDS latency stays hidden.
+template <class T, bool MASKED>
+__device__ __forceinline__ void pipelined_step(const char* kread, const char* vread,
+                                               WaveState<T>& ws, const AttnParams& p, float m_use,
+                                               int jn)
+{
+    constexpr int NB = T::NB, DBLK = T::DBLK;
+    constexpr int QK = T::KSTEPS * NB;   // QK^T MFMAs (t-major, block-minor)
+    constexpr int PV = 2 * NB * DBLK;    // P V MFMAs (b, u, d)
+    constexpr int PF = 2;                // read prefetch distance in slices
+    constexpr int EQ = 16 * NB / QK;     // exponentials per QK slice
+    constexpr int EP = 16 * NB / PV;     // score elements per P V slice
+    static_assert(EQ % 2 == 0 && EQ * QK == 16 * NB && EP * PV == 16 * NB, "slice split");
+
+    f32x16 sn[NB];
+    u32x4 pw[NB][2];
+    bf16x8 kop[QK];
+    s16x4 vlo[PV], vhi[PV];
+    float rs = 0.0f, mx = -__builtin_inff();
+
+    auto read_k = [&](int i) __attribute__((always_inline)) {
+        const int t = i / NB, b = i % NB;
+        kop[i] = *reinterpret_cast<const bf16x8*>(kread + 32 * b * T::ROWB + ws.kaddr[t]);
+    };
+    auto read_v = [&](int i) __attribute__((always_inline)) {
+        const int b = i / (2 * DBLK), u = (i / DBLK) % 2, d = i % DBLK;
+        const int kb = (32 * b + 16 * u) * T::ROWB;
+        vlo[i] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vread + kb + ws.vaddr[d][0]));
+        vhi[i] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vread + kb + ws.vaddr[d][1]));
+    };
+
+    static_for<PF>([&](auto ic) __attribute__((always_inline)) { read_k(ic.value); });
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<QK>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int i = ic.value, t = i / NB, b = i % NB;
+        if constexpr (t == 0)
+            sn[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[i], ws.qf[t], f32x16{}, 0, 0, 0);
+        else
+            sn[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[i], ws.qf[t], sn[b], 0, 0, 0);
+        if constexpr (i + PF < QK)
+            read_k(i + PF);
+        else
+            read_v(i + PF - QK);
+        static_for<EQ / 2>([&](auto kc) __attribute__((always_inline)) {
+            constexpr int el = i * EQ + 2 * kc.value, bb = el / 16, e = el % 16;
+            const float x0 = ws.s[bb][e], x1 = ws.s[bb][e + 1];
+            const float y0 = T::MODS ? x0 - m_use : __builtin_fmaf(x0, p.scale_log2, -m_use);
+            const float y1 = T::MODS ? x1 - m_use : __builtin_fmaf(x1, p.scale_log2, -m_use);
+            const float p0 = __builtin_amdgcn_exp2f(y0), p1 = __builtin_amdgcn_exp2f(y1);
+            rs += p0;
+            rs += p1;
+            pw[bb][e / 8][(e % 8) / 2] = pack_bf16(p0, p1);
+        });
+        __builtin_amdgcn_sched_barrier(0);
+    });
+    ws.l_run += rs;
+    static_for<PV>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int i = ic.value;
+        constexpr int b = i / (2 * DBLK), u = (i / DBLK) % 2, d = i % DBLK;
+        typedef short s16x8 __attribute__((ext_vector_type(8)));
+        s16x8 a8 = __builtin_shufflevector(vlo[i], vhi[i], 0, 1, 2, 3, 4, 5, 6, 7);
+        ws.oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a8),
+                                                             __builtin_bit_cast(bf16x8, pw[b][u]),
+                                                             ws.oacc[d], 0, 0, 0);
+        if constexpr (i + PF < PV) read_v(i + PF);
+        static_for<EP>([&](auto kc) __attribute__((always_inline)) {
+            constexpr int el = i * EP + kc.value, bb = el / 16, e = el % 16;
+            // element (bb, e) is key jn + 32bb + 8lh + e + (e >= 8 ? 8 : 0)
+            const int j = jn + 32 * bb + 8 * ws.lh + e + (e >= 8 ? 8 : 0);
+            float x = sn[bb][e];
+            if constexpr (T::MODS)
+                x = score_log2<T::SOFTCAP, T::ALIBI>(x, p.scale_log2, p.softcap_pre, p.softcap_post,
+                                                     ws.slope_log2, ws.ip, j);
+            if constexpr (MASKED)
+                if (j < ws.jlo || j > ws.jhi) x = -__builtin_inff();
+            sn[bb][e] = x;
+            mx = __builtin_fmaxf(mx, x);
+        });
+        __builtin_amdgcn_sched_barrier(0);
+    });
+    mx = pair_max(mx);
+    if constexpr (!T::MODS) mx *= p.scale_log2;  // raw max -> log2 units (scale > 0)
+    update_max(ws, mx);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) ws.s[b] = sn[b];
+}
+
+// The last step of the key loop: exponentials and P V of the current tile.
+template <class T>
+__device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, const AttnParams& p,
+                                          float m_use)
+{
+    u32x4 pw[T::NB][2];
+    exp_tile<T>(ws.s, pw, m_use, p.scale_log2, ws.l_run);
+    pv_tile<T>(vread, pw, ws);
+}
+
+template <class T>
 __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
 {
-    using C = Cfg<D>;
-    __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
+    constexpr int D = T::D, BN = T::BN;
+    // Separate LDS objects per buffer: the compiler can then prove that reads
+    // of one buffer do not alias the in-flight direct loads into another.
+    __shared__ __attribute__((aligned(1024))) char lds_k0[T::TILE];
+    __shared__ __attribute__((aligned(1024))) char lds_k1[T::TILE];
+    __shared__ __attribute__((aligned(1024))) char lds_v0[T::TILE];
+    __shared__ __attribute__((aligned(1024))) char lds_v1[T::TILE];
 
     const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int li = lane & 31, lh = lane >> 5;
 
     const WorkItem it = decode_block(p, blockIdx.x);
@@ -313,8 +477,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     const int hkv = it.hq / p.group;
 
     const __bf16* qb = static_cast<const __bf16*>(p.q);
-    const __bf16* kb = static_cast<const __bf16*>(p.k);
-    const __bf16* vb = static_cast<const __bf16*>(p.v);
+    const __bf16* kbase = static_cast<const __bf16*>(p.k);
+    const __bf16* vbase = static_cast<const __bf16*>(p.v);
     __bf16* ob = static_cast<__bf16*>(p.o);
     int64_t qoff, koff, voff, ooff;
     if (p.cu_q) {
@@ -328,86 +492,144 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         koff = (int64_t)it.b * p.sk_b + (int64_t)hkv * p.sk_h;
         voff = (int64_t)it.b * p.sv_b + (int64_t)hkv * p.sv_h;
     }
-    // Buffer ranges cover exactly the rows of this sequence and head.
-    auto rows_bytes = [](int rows, int64_t stride) -> uint32_t {
-        return rows <= 0 ? 0u : (uint32_t)((((int64_t)rows - 1) * stride + D) * 2);
-    };
-    const __amdgpu_buffer_rsrc_t qrs = make_rsrc(qb + qoff, rows_bytes(lq, p.sq_s));
-    const __amdgpu_buffer_rsrc_t krs = make_rsrc(kb + koff, rows_bytes(lk, p.sk_s));
-    const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vb + voff, rows_bytes(lk, p.sv_s));
+    kbase += koff;
+    vbase += voff;
 
-    // Q fragment (B operand): lane holds row q0 + 32*wave + li, dims 16t + 8lh .. +7.
+    WaveState<T> ws;
+    ws.lh = lh;
+    // Q fragment: lane holds row q0 + 32*wave + li, dims 16t + 8lh .. +7.
     const int qi = q0 + wave * 32 + li;
-    bf16x8 qf[C::KSTEPS];
+    {
+        uint32_t bytes = (uint32_t)((((int64_t)lq - 1) * p.sq_s + D) * 2);
+        __amdgpu_buffer_rsrc_t qrs = make_rsrc(qb + qoff, bytes);
 #pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t) {
-        uint32_t off = (uint32_t)(((int64_t)qi * p.sq_s + 16 * t + 8 * lh) * 2);
-        u32x4 raw = __builtin_amdgcn_raw_buffer_load_b128(qrs, off, 0, 0);
-        qf[t] = __builtin_bit_cast(bf16x8, raw);
+        for (int t = 0; t < T::KSTEPS; ++t) {
+            uint32_t off = (uint32_t)(((int64_t)qi * p.sq_s + 16 * t + 8 * lh) * 2);
+            ws.qf[t] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(qrs, off, 0, 0));
+        }
     }
+    // LDS read offsets (within a tile).
+    {
+        const int r = pi32(li);
+#pragma unroll
+        for (int t = 0; t < T::KSTEPS; ++t)
+            ws.kaddr[t] = r * T::ROWB + (((2 * t + lh) ^ chunk_swizzle<D>(r)) << 4);
+        const int g = lane >> 4, sl = lane & 15, a = sl & 3, f = sl >> 2;
+        const int sa = ((a & 1) << 1) | (a >> 1);  // head-dim order pi on O^T rows
+#pragma unroll
+        for (int d = 0; d < T::DBLK; ++d)
+#pragma unroll
+            for (int rr = 0; rr < 2; ++rr) {
+                int key = 8 * (g >> 1) + 4 * rr + f;
+                int dd = 32 * d + 16 * (g & 1) + 4 * sa;
+                ws.vaddr[d][rr] = key * T::ROWB + (((dd >> 3) ^ chunk_swizzle<D>(key)) << 4) +
+                                  (dd & 7) * 2;
+            }
+    }
+    const uint32_t klp = load_lane_offset<T>(wave, lane, p.sk_s);
+    const uint32_t vlp = load_lane_offset<T>(wave, lane, p.sv_s);
 
     // Visible key interval of this lane's row; rows past the end see nothing.
-    int jlo = 1, jhi = 0;
-    if (qi < lq) band_row(p.band, qi, lq, lk, &jlo, &jhi);
-    const int ip = qi + (lk - lq);
-    float slope_log2 = 0.0f;
-    if constexpr (ALIBI) slope_log2 = p.slopes[it.hq] * kLog2e;
+    ws.jlo = 1;
+    ws.jhi = 0;
+    if (qi < lq) band_row(p.band, qi, lq, lk, &ws.jlo, &ws.jhi);
+    ws.ip = qi + (lk - lq);
+    ws.slope_log2 = 0.0f;
+    if constexpr (T::ALIBI) ws.slope_log2 = p.slopes[it.hq] * kLog2e;
+
+#pragma unroll
+    for (int d = 0; d < T::DBLK; ++d) ws.oacc[d] = f32x16{};
+    ws.m_run = -__builtin_inff();
+    ws.l_run = 0.0f;
+    ws.alpha = 1.0f;
+    ws.need = false;
 
     const TilePlan gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
-    const TilePlan wp = plan_tiles(p.band, q0 + wave * 32, 32, lq, lk, BN);
+    const int lo = gp.lo, hi = gp.hi;
+    auto masked = [&](int j) __attribute__((always_inline)) { return !(j >= gp.full_lo && j < gp.full_hi); };
 
-    f32x16 oacc[C::DBLK];
-#pragma unroll
-    for (int d = 0; d < C::DBLK; ++d)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) oacc[d][e] = 0.0f;
-    float m_run = -__builtin_inff();
-    float l_run = 0.0f;
-
-    if (gp.hi > gp.lo) {
-        TileRegs<D> regs;
-        load_tile<D>(regs, krs, vrs, gp.lo * BN, p.sk_s, p.sv_s, tid);
-        store_tile<D>(regs, smem, tid);
+    if (hi > lo) {
+        // Prologue: K_lo, V_lo -> buffers 0, K_lo+1 -> K buffer 1; S_lo.
+        issue_tile<T>(lds_k0, kbase, lo * BN, lk, p.sk_s, klp, wave);
+        issue_tile<T>(lds_v0, vbase, lo * BN, lk, p.sv_s, vlp, wave);
+        if (lo + 1 < hi) issue_tile<T>(lds_k1, kbase, (lo + 1) * BN, lk, p.sk_s, klp, wave);
+        __builtin_amdgcn_s_waitcnt(0);  // this thread's loads have landed in LDS
         __syncthreads();
-        int stage = 0;
-        for (int kt = gp.lo; kt < gp.hi; ++kt) {
-            const bool has_next = kt + 1 < gp.hi;
-            if (has_next) load_tile<D>(regs, krs, vrs, (kt + 1) * BN, p.sk_s, p.sv_s, tid);
-            const char* st = smem + stage * C::STAGE;
-            const bool active = kt >= wp.lo && kt < wp.hi;
-            if (active) {
-                const bool masked = !(kt >= wp.full_lo && kt < wp.full_hi);
-                if (masked)
-                    tile_step<D, SOFTCAP, ALIBI, true>(st, qf, oacc, m_run, l_run, p, kt * BN, li, lh,
-                                                       jlo, jhi, ip, slope_log2);
-                else
-                    tile_step<D, SOFTCAP, ALIBI, false>(st, qf, oacc, m_run, l_run, p, kt * BN, li, lh,
-                                                        jlo, jhi, ip, slope_log2);
-            }
-            if (has_next) store_tile<D>(regs, smem + (stage ^ 1) * C::STAGE, tid);
+        qk_tile<T>(lds_k0, ws, ws.s);
+        const bool masked_lo = !(lo >= gp.full_lo && lo < gp.full_hi);
+        float mx = masked_lo ? mods_and_max<T, true>(ws.s, p, ws, lo * BN)
+                             : mods_and_max<T, false>(ws.s, p, ws, lo * BN);
+        update_max(ws, mx);
+        __syncthreads();  // K buffer 0 is reloaded in the first iteration
+
+        // Iteration j with parity PAR = (j - lo) & 1 reads K_{j+1} from K
+        // buffer PAR^1 and V_j from V buffer PAR, and loads K_{j+2} into K
+        // buffer PAR and V_{j+1} into V buffer PAR^1. MASKED is the class of
+        // tile j+1.
+        auto iteration = [&](auto par_c, auto masked_c, int j) __attribute__((always_inline)) {
+            constexpr int PAR = decltype(par_c)::value;
+            constexpr bool MASKED = decltype(masked_c)::value;
+            char* kread = PAR ? lds_k0 : lds_k1;
+            char* kwrite = PAR ? lds_k1 : lds_k0;
+            char* vread = PAR ? lds_v1 : lds_v0;
+            char* vwrite = PAR ? lds_v0 : lds_v1;
+            rescale_if_needed(ws);
+            if (j + 2 < hi) issue_tile<T>(kwrite, kbase, (j + 2) * BN, lk, p.sk_s, klp, wave);
+            issue_tile<T>(vwrite, vbase, (j + 1) * BN, lk, p.sv_s, vlp, wave);
+            const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
+            pipelined_step<T, MASKED>(kread, vread, ws, p, m_use, (j + 1) * BN);
+            __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
-            stage ^= 1;
-        }
+        };
+        // Loop splitting (Section 3.4): leading partial tiles, check-free full
+        // tiles, trailing partial tiles; each phase has a branch-free body.
+        int j = lo, par = 0;
+        auto phase = [&](auto masked_c, int end) __attribute__((always_inline)) {  // iterations while tile j+1 < end
+            if (par && j + 1 < end) {
+                iteration(Parity<1>{}, masked_c, j);
+                ++j;
+                par = 0;
+            }
+            while (j + 2 < end) {
+                iteration(Parity<0>{}, masked_c, j);
+                iteration(Parity<1>{}, masked_c, j + 1);
+                j += 2;
+            }
+            if (j + 1 < end) {
+                iteration(Parity<0>{}, masked_c, j);
+                ++j;
+                par = 1;
+            }
+        };
+        phase(Bool<true>{}, gp.full_lo);
+        phase(Bool<false>{}, gp.full_hi);
+        phase(Bool<true>{}, hi);
+        rescale_if_needed(ws);
+        const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
+        if (par)
+            last_step<T>(lds_v1, ws, p, m_use);
+        else
+            last_step<T>(lds_v0, ws, p, m_use);
     }
 
     // Epilogue: O = O^T / l, LSE = (m + log2 l) ln 2. Lane halves hold halves of the row sum.
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_tot = pair_sum(ws.l_run);
     if (qi < lq) {
         const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
         __bf16* orow = ob + ooff + (int64_t)qi * p.so_s;
 #pragma unroll
-        for (int d = 0; d < C::DBLK; ++d) {
+        for (int d = 0; d < T::DBLK; ++d) {
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 u32x4 w;
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                    w[q] = pack_bf16(oacc[d][8 * u + 2 * q] * inv, oacc[d][8 * u + 2 * q + 1] * inv);
+                    w[q] = pack_bf16(ws.oacc[d][8 * u + 2 * q] * inv, ws.oacc[d][8 * u + 2 * q + 1] * inv);
                 *reinterpret_cast<u32x4*>(orow + 32 * d + 16 * u + 8 * lh) = w;
             }
         }
         if (p.lse && lh == 0) {
-            float lse = l_tot > 0.0f ? (m_run + __builtin_log2f(l_tot)) * kLn2 : -__builtin_inff();
+            float lse = l_tot > 0.0f ? (ws.m_run + __builtin_log2f(l_tot)) * kLn2 : -__builtin_inff();
             int64_t idx = p.cu_q ? (int64_t)it.hq * p.total_q + qrow0 + qi
                                  : ((int64_t)it.b * p.hq + it.hq) * lq + qi;
             p.lse[idx] = lse;
@@ -415,12 +637,23 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     }
 }
 
+// Keys per tile: 32 at head dim 128 keeps the double-buffered scores of the
+// pipeline within the 256 registers of two waves per SIMD; 64 at head dim 64.
+constexpr int key_tile_width(int d)
+{
+#ifdef ATTN_BN
+    return ATTN_BN;
+#else
+    return d == 128 ? 32 : 64;
+#endif
+}
+
 template <int D, bool SOFTCAP, bool ALIBI>
 hipError_t launch(const AttnParams& p, hipStream_t stream)
 {
+    using T = Traits<D, key_tile_width(D), SOFTCAP, ALIBI>;
     int64_t blocks = (int64_t)p.num_q_tiles * p.hq * p.batch;
-    hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, SOFTCAP, ALIBI>), dim3((unsigned)blocks), dim3(NT),
-                       0, stream, p);
+    hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)blocks), dim3(NT), 0, stream, p);
     return hipGetLastError();
 }
 
