@@ -57,9 +57,6 @@ constexpr int BM = 128;      // query rows per workgroup
 constexpr int NT = 256;      // threads per workgroup (4 waves)
 constexpr float TAU = 8.0f;  // lazy-rescale threshold, log2 units
 
-// Instruction classes for __builtin_amdgcn_sched_group_barrier.
-constexpr int SG_VALU = 0x2, SG_MFMA = 0x8, SG_DS_READ = 0x100, SG_TRANS = 0x400;
-
 template <int D_, int BN_, bool SOFTCAP_, bool ALIBI_>
 struct Traits {
     static constexpr int D = D_, BN = BN_;
@@ -115,20 +112,19 @@ __device__ __forceinline__ uint32_t load_lane_offset(int wave, int lane, int64_t
     return (uint32_t)(((int64_t)row * stride + 8 * c) * 2);
 }
 
-// Issue the direct global->LDS loads of one tile (rows j0..j0+BN-1 of a slice
-// whose first row is at `base`; rows at or past `rows` read as zero).
+// Issue the direct global->LDS loads of one tile: rows j0..j0+BN-1 of the
+// slice described by `rs` (whose range ends at the sequence end, so rows past
+// it read as zero). The row offset is wave-uniform and added to the lane's
+// constant byte offset.
 template <class T>
-__device__ __forceinline__ void issue_tile(char* lds_tile, const __bf16* base, int j0, int rows,
-                                           int64_t stride, uint32_t lane_off, int wave)
+__device__ __forceinline__ void issue_tile(char* lds_tile, __amdgpu_buffer_rsrc_t rs, int j0,
+                                           uint32_t row_bytes, uint32_t lane_off, int wave)
 {
 #pragma unroll
     for (int p = 0; p < T::LOADS; ++p) {
-        const int r0 = j0 + p * T::ROWS_PER_LOAD;
-        const int left = rows - r0;
-        const uint32_t bytes = left <= 0 ? 0u : (uint32_t)((((int64_t)left - 1) * stride + T::D) * 2);
-        __amdgpu_buffer_rsrc_t rs = make_rsrc(base + (int64_t)r0 * stride, bytes);
+        const uint32_t off = lane_off + (uint32_t)(j0 + p * T::ROWS_PER_LOAD) * row_bytes;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rs, (lds_void*)(lds_tile + (4 * p + wave) * 1024), 16, lane_off, 0, 0, 0);
+            rs, (lds_void*)(lds_tile + (4 * p + wave) * 1024), 16, off, 0, 0, 0);
     }
 }
 
@@ -528,6 +524,13 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     }
     const uint32_t klp = load_lane_offset<T>(wave, lane, p.sk_s);
     const uint32_t vlp = load_lane_offset<T>(wave, lane, p.sv_s);
+    // One buffer descriptor per K/V slice; its range ends at the sequence end.
+    auto slice_bytes = [&](int64_t stride) {
+        return lk <= 0 ? 0u : (uint32_t)((((int64_t)lk - 1) * stride + D) * 2);
+    };
+    const __amdgpu_buffer_rsrc_t krs = make_rsrc(kbase, slice_bytes(p.sk_s));
+    const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vbase, slice_bytes(p.sv_s));
+    const uint32_t krow = (uint32_t)(p.sk_s * 2), vrow = (uint32_t)(p.sv_s * 2);
 
     // Visible key interval of this lane's row; rows past the end see nothing.
     ws.jlo = 1;
@@ -546,13 +549,12 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
 
     const TilePlan gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
     const int lo = gp.lo, hi = gp.hi;
-    auto masked = [&](int j) __attribute__((always_inline)) { return !(j >= gp.full_lo && j < gp.full_hi); };
 
     if (hi > lo) {
         // Prologue: K_lo, V_lo -> buffers 0, K_lo+1 -> K buffer 1; S_lo.
-        issue_tile<T>(lds_k0, kbase, lo * BN, lk, p.sk_s, klp, wave);
-        issue_tile<T>(lds_v0, vbase, lo * BN, lk, p.sv_s, vlp, wave);
-        if (lo + 1 < hi) issue_tile<T>(lds_k1, kbase, (lo + 1) * BN, lk, p.sk_s, klp, wave);
+        issue_tile<T>(lds_k0, krs, lo * BN, krow, klp, wave);
+        issue_tile<T>(lds_v0, vrs, lo * BN, vrow, vlp, wave);
+        if (lo + 1 < hi) issue_tile<T>(lds_k1, krs, (lo + 1) * BN, krow, klp, wave);
         __builtin_amdgcn_s_waitcnt(0);  // this thread's loads have landed in LDS
         __syncthreads();
         qk_tile<T>(lds_k0, ws, ws.s);
@@ -574,8 +576,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             char* vread = PAR ? lds_v1 : lds_v0;
             char* vwrite = PAR ? lds_v0 : lds_v1;
             rescale_if_needed(ws);
-            if (j + 2 < hi) issue_tile<T>(kwrite, kbase, (j + 2) * BN, lk, p.sk_s, klp, wave);
-            issue_tile<T>(vwrite, vbase, (j + 1) * BN, lk, p.sv_s, vlp, wave);
+            if (j + 2 < hi) issue_tile<T>(kwrite, krs, (j + 2) * BN, krow, klp, wave);
+            issue_tile<T>(vwrite, vrs, (j + 1) * BN, vrow, vlp, wave);
             const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
             pipelined_step<T, MASKED>(kread, vread, ws, p, m_use, (j + 1) * BN);
             __builtin_amdgcn_s_waitcnt(0);
@@ -637,14 +639,15 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     }
 }
 
-// Keys per tile: 32 at head dim 128 keeps the double-buffered scores of the
-// pipeline within the 256 registers of two waves per SIMD; 64 at head dim 64.
-constexpr int key_tile_width(int d)
+// Keys per tile. 64 halves the per-tile barrier, load-wait and max-exchange
+// overhead relative to 32 and still fits the pipeline's double-buffered
+// scores in the registers of two waves per SIMD.
+constexpr int key_tile_width(int)
 {
 #ifdef ATTN_BN
     return ATTN_BN;
 #else
-    return d == 128 ? 32 : 64;
+    return 64;
 #endif
 }
 
