@@ -216,7 +216,7 @@ struct WaveState {
     int kaddr[T::KSTEPS];      // LDS byte offsets of this lane's K reads
     int vaddr[T::DBLK][2];     // LDS byte offsets of this lane's V transpose reads
     f32x16 oacc[T::DBLK];      // O^T accumulator
-    f32x16 s[T::NB];           // scores of the current tile
+    f32x16 sa[T::NB], sb[T::NB];  // scores of tiles of even / odd parity
     float m_run, l_run, alpha;
     bool need;
     // row constants
@@ -347,8 +347,9 @@ __device__ __forceinline__ void pv_tile(const char* vt, const u32x4 (&pw)[T::NB]
 // runs while the matrix cores are busy and LDS latency stays hidden.
 template <class T, bool MASKED>
 __device__ __forceinline__ void pipelined_step(const char* kread, const char* vread,
-                                               WaveState<T>& ws, const AttnParams& p, float m_use,
-                                               int jn)
+                                               WaveState<T>& ws, const f32x16 (&sc)[T::NB],
+                                               f32x16 (&sn)[T::NB], const AttnParams& p,
+                                               float m_use, int jn)
 {
     constexpr int NB = T::NB, DBLK = T::DBLK;
     constexpr int QK = T::KSTEPS * NB;   // QK^T MFMAs (t-major, block-minor)
@@ -358,7 +359,6 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     constexpr int EP = 16 * NB / PV;     // score elements per P V slice
     static_assert(EQ % 2 == 0 && EQ * QK == 16 * NB && EP * PV == 16 * NB, "slice split");
 
-    f32x16 sn[NB];
     u32x4 pw[NB][2];
     bf16x8 kop[QK];
     s16x4 vlo[PV], vhi[PV];
@@ -389,7 +389,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             read_v(i + PF - QK);
         static_for<EQ / 2>([&](auto kc) __attribute__((always_inline)) {
             constexpr int el = i * EQ + 2 * kc.value, bb = el / 16, e = el % 16;
-            const float x0 = ws.s[bb][e], x1 = ws.s[bb][e + 1];
+            const float x0 = sc[bb][e], x1 = sc[bb][e + 1];
             const float y0 = T::MODS ? x0 - m_use : __builtin_fmaf(x0, p.scale_log2, -m_use);
             const float y1 = T::MODS ? x1 - m_use : __builtin_fmaf(x1, p.scale_log2, -m_use);
             const float p0 = __builtin_amdgcn_exp2f(y0), p1 = __builtin_amdgcn_exp2f(y1);
@@ -427,17 +427,15 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     mx = pair_max(mx);
     if constexpr (!T::MODS) mx *= p.scale_log2;  // raw max -> log2 units (scale > 0)
     update_max(ws, mx);
-#pragma unroll
-    for (int b = 0; b < NB; ++b) ws.s[b] = sn[b];
 }
 
 // The last step of the key loop: exponentials and P V of the current tile.
 template <class T>
-__device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, const AttnParams& p,
-                                          float m_use)
+__device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, f32x16 (&sc)[T::NB],
+                                          const AttnParams& p, float m_use)
 {
     u32x4 pw[T::NB][2];
-    exp_tile<T>(ws.s, pw, m_use, p.scale_log2, ws.l_run);
+    exp_tile<T>(sc, pw, m_use, p.scale_log2, ws.l_run);
     pv_tile<T>(vread, pw, ws);
 }
 
@@ -557,10 +555,10 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         if (lo + 1 < hi) issue_tile<T>(lds_k1, krs, (lo + 1) * BN, krow, klp, wave);
         __builtin_amdgcn_s_waitcnt(0);  // this thread's loads have landed in LDS
         __syncthreads();
-        qk_tile<T>(lds_k0, ws, ws.s);
+        qk_tile<T>(lds_k0, ws, ws.sa);
         const bool masked_lo = !(lo >= gp.full_lo && lo < gp.full_hi);
-        float mx = masked_lo ? mods_and_max<T, true>(ws.s, p, ws, lo * BN)
-                             : mods_and_max<T, false>(ws.s, p, ws, lo * BN);
+        float mx = masked_lo ? mods_and_max<T, true>(ws.sa, p, ws, lo * BN)
+                             : mods_and_max<T, false>(ws.sa, p, ws, lo * BN);
         update_max(ws, mx);
         __syncthreads();  // K buffer 0 is reloaded in the first iteration
 
@@ -579,7 +577,10 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             if (j + 2 < hi) issue_tile<T>(kwrite, krs, (j + 2) * BN, krow, klp, wave);
             issue_tile<T>(vwrite, vrs, (j + 1) * BN, vrow, vlp, wave);
             const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
-            pipelined_step<T, MASKED>(kread, vread, ws, p, m_use, (j + 1) * BN);
+            if constexpr (PAR == 0)
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, (j + 1) * BN);
+            else
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, (j + 1) * BN);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
         };
@@ -609,9 +610,9 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         rescale_if_needed(ws);
         const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
         if (par)
-            last_step<T>(lds_v1, ws, p, m_use);
+            last_step<T>(lds_v1, ws, ws.sb, p, m_use);
         else
-            last_step<T>(lds_v0, ws, p, m_use);
+            last_step<T>(lds_v0, ws, ws.sa, p, m_use);
     }
 
     // Epilogue: O = O^T / l, LSE = (m + log2 l) ln 2. Lane halves hold halves of the row sum.
