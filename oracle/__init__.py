@@ -19,6 +19,8 @@ _SRC = os.path.join(_HERE, "attn_ref.c")
 _LIB = os.path.join(_HERE, "libattn_ref.so")
 
 MASK_NONE, MASK_CAUSAL, MASK_SLIDING_WINDOW = 0, 1, 2
+MASK_PREFIX_LM, MASK_GLOBAL_WINDOW, MASK_SHARE_QUESTION, MASK_CAUSAL_BLOCKWISE = 3, 4, 5, 6
+NORM_SOFTMAX, NORM_RELU, NORM_SIGMOID = 0, 1, 2
 
 
 class _RefParams(ctypes.Structure):
@@ -37,6 +39,13 @@ class _RefParams(ctypes.Structure):
         ("softcap", ctypes.c_double),
         ("cu_q", ctypes.POINTER(ctypes.c_int32)),
         ("cu_k", ctypes.POINTER(ctypes.c_int32)),
+        ("prefix_len", ctypes.c_int32),
+        ("relpos", ctypes.c_int32),
+        ("norm_kind", ctypes.c_int32),
+        ("token_ids", ctypes.POINTER(ctypes.c_int32)),
+        ("query_start", ctypes.c_int32),
+        ("global_tokens", ctypes.POINTER(ctypes.c_int32)),
+        ("num_global", ctypes.c_int32),
     ]
 
 
@@ -104,13 +113,19 @@ def _i32(x) -> np.ndarray:
 def attention(q, k, v, *, scale: float, mask: int = MASK_NONE, window_left: int = -1,
               window_right: int = -1, slopes=None, softcap: float = 0.0,
               cu_seqlens_q=None, cu_seqlens_k=None, rows=None, want_probs: bool = False,
-              lib=None):
+              prefix_len: int = 0, relpos: bool = False, norm: int = NORM_SOFTMAX,
+              token_ids=None, query_start: int = 0, global_tokens=None, lib=None):
     """Reference attention forward.
 
     Fixed length: q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] -> o [B,Hq,Sq,D], lse [B,Hq,Sq].
     Varlen (cu_seqlens given): q [Tq,Hq,D], k/v [Tk,Hkv,D] -> o [Tq,Hq,D], lse [Hq,Tq].
     `rows`: optional flat LSE indices to compute; other rows are left NaN.
-    Returns (o, lse) as float64 numpy arrays, plus P [B,Hq,Sq,Sk] if want_probs.
+    PrefixLM uses `prefix_len`; the share-question and causal-blockwise masks
+    use `token_ids` (one id per key position; blockwise also `query_start`);
+    the global sliding window uses the window bounds and `global_tokens`.
+    `norm` selects softmax, ReLU(S)/L or Sigmoid(S)/L (the last two have no
+    LSE: NaN). Returns (o, lse) as float64 numpy arrays, plus P [B,Hq,Sq,Sk]
+    if want_probs.
     """
     lib = lib or load()
     qn, kn, vn = _f32(q), _f32(k), _f32(v)
@@ -134,6 +149,19 @@ def attention(q, k, v, *, scale: float, mask: int = MASK_NONE, window_left: int 
     p.mask_kind = int(mask)
     p.window_left, p.window_right = int(window_left), int(window_right)
     p.softcap = float(softcap)
+    p.prefix_len = int(prefix_len)
+    p.relpos = 1 if relpos else 0
+    p.norm_kind = int(norm)
+    p.query_start = int(query_start)
+    ids = None
+    if token_ids is not None:
+        ids = _i32(token_ids)
+        p.token_ids = ids.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    gl = None
+    if global_tokens is not None:
+        gl = _i32(global_tokens)
+        p.global_tokens = gl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        p.num_global = int(gl.size)
     sl = None
     if slopes is not None:
         sl = np.ascontiguousarray(np.asarray(_f32(slopes), dtype=np.float64))
@@ -156,7 +184,7 @@ def attention(q, k, v, *, scale: float, mask: int = MASK_NONE, window_left: int 
                           probs.ctypes.data if probs is not None else None)
     if rc != 0:
         raise ValueError("oracle rejected its parameters")
-    del sl
+    del sl, ids, gl
     if want_probs:
         return o, lse, probs
     return o, lse
@@ -169,4 +197,4 @@ def attention_inputs(inp, rows=None, **kw):
                      window_left=wl.window_left, window_right=wl.window_right,
                      slopes=inp.slopes, softcap=wl.softcap,
                      cu_seqlens_q=inp.cu_seqlens, cu_seqlens_k=inp.cu_seqlens,
-                     rows=rows, **kw)
+                     rows=rows, **{**inp.oracle_mask_kwargs(), **kw})

@@ -7,8 +7,11 @@ their inputs from here without sharing any of the method.
 The paper measures on model-shaped random tensors (Section 4.1, "Benchmark
 Configurations": head tuples query/kv/head-dim such as 32/32/128, 64/8/128,
 128/8/128, sequence lengths 1k-8k at 16k tokens per batch) and fixes no value
-distribution. The five workloads below keep that shape family and add the
-variants of Appendix A that this library implements.
+distribution. The five headline workloads keep that shape family and add the
+variants of Appendix A built in first; the further variants (PrefixLM,
+relative position, ReLU / Sigmoid normalisation, their combination, global
+sliding window, share question, causal blockwise) each get one workload at
+the Llama2-7B tuple 32/32/128 with S = 8k and B = 2 (16k tokens).
 
 Input recipe (identical on every machine because it uses the CPU generator):
     g = torch.Generator().manual_seed(seed)
@@ -16,6 +19,9 @@ Input recipe (identical on every machine because it uses the CPU generator):
     q, k, v = torch.randn(shape, generator=g) * sigma, drawn in that order
     bf16 workloads round the fp32 draw to bfloat16 (round-to-nearest-even).
 ALiBi slopes are inputs too: slope_h = 2 ** (-8 h / H) for h = 1..H.
+Segment starts (share question, causal blockwise) are drawn after v from the
+same generator: num_segments - 1 distinct cut points, sorted, inside the
+response region (prompt_len, S) or the document region (0, query_start).
 """
 from __future__ import annotations
 
@@ -28,6 +34,14 @@ import torch
 MASK_NONE = 0
 MASK_CAUSAL = 1
 MASK_SLIDING_WINDOW = 2
+MASK_PREFIX_LM = 3
+MASK_GLOBAL_WINDOW = 4
+MASK_SHARE_QUESTION = 5
+MASK_CAUSAL_BLOCKWISE = 6
+MASK_NAMES = {MASK_NONE: "none", MASK_CAUSAL: "causal", MASK_SLIDING_WINDOW: "sliding_window",
+              MASK_PREFIX_LM: "prefix_lm", MASK_GLOBAL_WINDOW: "global_sliding_window",
+              MASK_SHARE_QUESTION: "share_question", MASK_CAUSAL_BLOCKWISE: "causal_blockwise"}
+NORM_CODES = {"softmax": 0, "relu": 1, "sigmoid": 2}
 
 
 @dataclasses.dataclass(frozen=True)
@@ -49,6 +63,12 @@ class Workload:
     varlen: bool = False
     len_lo: int = 0            # varlen: lengths uniform in [len_lo, len_hi]
     len_hi: int = 0
+    prefix_len: int = 0        # PrefixLM L_p; share question: prompt length
+    num_global: int = 0        # global sliding window: positions 0..num_global-1
+    num_segments: int = 0      # share question responses / blockwise documents
+    query_start: int = 0       # causal blockwise L_q
+    relpos: bool = False       # relative position term (i - j)
+    norm: str = "softmax"      # "softmax", "relu" or "sigmoid"
 
     @property
     def scale(self) -> float:
@@ -74,9 +94,31 @@ WORKLOADS = {
                                 len_lo=256, len_hi=8192),
 }
 
-# Order used when a list of all five is wanted.
+def _llama7b(name, seed, **kw):
+    return Workload(name, "bf16", 2, 32, 32, 8192, 128, seed=seed, **kw)
+
+
+# Further variants of Appendix A, one workload each (Llama2-7B tuple, 16k tokens).
+NEXT_WORKLOADS = {
+    "prefixlm_bf16": _llama7b("prefixlm_bf16", 5, mask=MASK_PREFIX_LM, prefix_len=2048),
+    "relpos_bf16": _llama7b("relpos_bf16", 6, mask=MASK_CAUSAL, relpos=True),
+    "relu_bf16": _llama7b("relu_bf16", 7, mask=MASK_CAUSAL, norm="relu"),
+    "sigmoid_bf16": _llama7b("sigmoid_bf16", 8, mask=MASK_CAUSAL, norm="sigmoid"),
+    "combo_bf16": _llama7b("combo_bf16", 9, mask=MASK_PREFIX_LM, prefix_len=2048,
+                           softcap=50.0, norm="sigmoid"),
+    "global_window_bf16": _llama7b("global_window_bf16", 10, mask=MASK_GLOBAL_WINDOW,
+                                   window_left=512, window_right=512, num_global=16),
+    "share_question_bf16": _llama7b("share_question_bf16", 11, mask=MASK_SHARE_QUESTION,
+                                    prefix_len=2048, num_segments=4),
+    "causal_blockwise_bf16": _llama7b("causal_blockwise_bf16", 12, mask=MASK_CAUSAL_BLOCKWISE,
+                                      num_segments=8, query_start=6144),
+}
+WORKLOADS.update(NEXT_WORKLOADS)
+
+# Order used when a list of the five headline workloads is wanted.
 WORKLOAD_ORDER = ["plain_fp32", "causal_bf16", "gqa_swa_bf16",
                   "alibi_softcap_bf16", "varlen_gqa_bf16"]
+NEXT_ORDER = list(NEXT_WORKLOADS)
 
 
 @dataclasses.dataclass
@@ -90,6 +132,7 @@ class Inputs:
     slopes: Optional[torch.Tensor]       # fp32 [Hq] or None
     cu_seqlens: Optional[torch.Tensor]   # int32 [B+1] or None
     lengths: Optional[list]
+    segment_starts: Optional[torch.Tensor] = None  # int32 [num_segments] or None
 
     @property
     def max_seqlen(self) -> int:
@@ -102,6 +145,44 @@ class Inputs:
         if self.lengths is None:
             return self.wl.batch * self.wl.seqlen
         return sum(self.lengths)
+
+    def variant_kwargs(self, device=None) -> dict:
+        """Keyword arguments of paper_2605_05023_amd.fwd / make_desc for this
+        workload's variant (tensors moved to `device`)."""
+        wl = self.wl
+        kw = dict(mask=MASK_NAMES[wl.mask], softcap=wl.softcap, scale=wl.scale,
+                  prefix_len=wl.prefix_len, num_global=wl.num_global,
+                  query_start=wl.query_start, relative_position=wl.relpos, norm=wl.norm)
+        if wl.mask in (MASK_SLIDING_WINDOW, MASK_GLOBAL_WINDOW):
+            kw["window"] = (wl.window_left, wl.window_right)
+        if self.slopes is not None:
+            kw["alibi_slopes"] = self.slopes.to(device) if device is not None else self.slopes
+        if self.segment_starts is not None:
+            seg = self.segment_starts
+            kw["segment_starts"] = seg.to(device) if device is not None else seg
+        if self.cu_seqlens is not None:
+            cu = self.cu_seqlens.to(device) if device is not None else self.cu_seqlens
+            kw.update(cu_seqlens_q=cu, cu_seqlens_k=cu, max_seqlen_q=self.max_seqlen,
+                      max_seqlen_k=self.max_seqlen)
+        return kw
+
+    def oracle_mask_kwargs(self) -> dict:
+        """The same variant in the CPU oracle's vocabulary: one segment id per
+        key position (largest k with start_k <= position, -1 before the first
+        start) and the global positions as a list."""
+        wl = self.wl
+        kw = dict(prefix_len=wl.prefix_len, relpos=wl.relpos, norm=NORM_CODES[wl.norm],
+                  query_start=wl.query_start)
+        if wl.mask == MASK_GLOBAL_WINDOW:
+            kw["global_tokens"] = list(range(wl.num_global))
+        if self.segment_starts is not None:
+            S = self.max_seqlen
+            ids = [-1] * S
+            for k, st in enumerate(self.segment_starts.tolist()):
+                for pos in range(st, S):
+                    ids[pos] = k
+            kw["token_ids"] = ids
+        return kw
 
 
 def alibi_slopes(nheads: int) -> torch.Tensor:
@@ -149,4 +230,12 @@ def make_inputs(wl: Workload, *, lengths=None, seqlen=None, batch=None,
         wl = dataclasses.replace(wl, batch=len(lengths) if wl.varlen else B,
                                  seqlen=0 if wl.varlen else (wl.seqlen if seqlen is None else seqlen))
     slopes = alibi_slopes(wl.hq) if wl.alibi else None
-    return Inputs(wl, q, k, v, slopes, cu, lengths)
+    seg = None
+    if wl.mask in (MASK_SHARE_QUESTION, MASK_CAUSAL_BLOCKWISE):
+        S = max(lengths) if wl.varlen else wl.seqlen
+        lo = wl.prefix_len if wl.mask == MASK_SHARE_QUESTION else 0
+        hi = S if wl.mask == MASK_SHARE_QUESTION else min(wl.query_start, S)
+        n = max(1, min(wl.num_segments, hi - lo))
+        cuts = (torch.randperm(max(hi - lo - 1, 0), generator=g)[:n - 1] + lo + 1).tolist()
+        seg = torch.tensor(sorted([lo] + cuts), dtype=torch.int32)
+    return Inputs(wl, q, k, v, slopes, cu, lengths, seg)

@@ -24,7 +24,12 @@ import oracle
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_cases.yaml")
 _NS = {"ln": math.log, "exp": math.exp, "e": math.e, "inf": math.inf, "sqrt": math.sqrt}
 _MASKS = {"none": oracle.MASK_NONE, "causal": oracle.MASK_CAUSAL,
-          "window": oracle.MASK_SLIDING_WINDOW}
+          "window": oracle.MASK_SLIDING_WINDOW, "prefix_lm": oracle.MASK_PREFIX_LM,
+          "global_window": oracle.MASK_GLOBAL_WINDOW,
+          "share_question": oracle.MASK_SHARE_QUESTION,
+          "causal_blockwise": oracle.MASK_CAUSAL_BLOCKWISE}
+_NORMS = {"softmax": oracle.NORM_SOFTMAX, "relu": oracle.NORM_RELU,
+          "sigmoid": oracle.NORM_SIGMOID}
 
 
 def _val(x):
@@ -59,7 +64,13 @@ def _run_case(lib, c):
     kw = dict(scale=_val(c["scale"]), mask=_MASKS[c["mask"]],
               window_left=int(c.get("window_left", -1)),
               window_right=int(c.get("window_right", -1)),
-              softcap=_val(c.get("softcap", 0)), lib=lib)
+              softcap=_val(c.get("softcap", 0)), lib=lib,
+              norm=_NORMS[c.get("norm", "softmax")], prefix_len=int(c.get("prefix_len", 0)),
+              relpos=bool(c.get("relpos", 0)), query_start=int(c.get("query_start", 0)))
+    if "token_ids" in c:
+        kw["token_ids"] = np.array(c["token_ids"], dtype=np.int32)
+    if "global_tokens" in c:
+        kw["global_tokens"] = np.array(c["global_tokens"], dtype=np.int32)
     if "slopes" in c:
         kw["slopes"] = np.array(_val(c["slopes"]), dtype=np.float32)
     if "cu" in c:
@@ -79,7 +90,10 @@ def pin_hand_cases(lib):
     for c in load_hand_cases():
         o, lse = _run_case(lib, c)
         _close(o, _val(c["o"]), 2e-6, c["name"] + " O")
-        _close(lse, _val(c["lse"]), 2e-6, c["name"] + " LSE")
+        if "lse" in c:
+            _close(lse, _val(c["lse"]), 2e-6, c["name"] + " LSE")
+        else:  # ReLU / Sigmoid define no normaliser
+            assert np.isnan(np.asarray(lse)).all(), c["name"] + ": LSE must be NaN"
 
 
 def _rand(shape, seed, scale=1.0):
@@ -321,10 +335,185 @@ def pin_row_subset(lib):
     assert np.isnan(np.delete(ls.reshape(-1), rows)).all()
 
 
+def _zero_q_counts(lib, S, visible_sets, what, **kw):
+    """Q = 0: O_i = mean of the visible V rows, LSE_i = ln n_i (O = 0, LSE = -inf
+    for an empty row). visible_sets[i] is the set of keys row i must see."""
+    D = 3
+    v = _rand((1, 1, S, D), 40)
+    q = torch.zeros((1, 1, S, D))
+    k = _rand((1, 1, S, D), 41)
+    o, lse = oracle.attention(q, k, v, scale=1.0, lib=lib, **kw)
+    vn = v[0, 0].double().numpy()
+    for i in range(S):
+        js = sorted(visible_sets[i])
+        if not js:
+            _close(o[0, 0, i], np.zeros(D), 0.0, f"{what}: empty row {i} O")
+            _close(lse[0, 0, i], -math.inf, 0.0, f"{what}: empty row {i} LSE")
+            continue
+        _close(o[0, 0, i], vn[js].mean(0), 1e-12, f"{what}: row {i} O")
+        _close(lse[0, 0, i], math.log(len(js)), 1e-12, f"{what}: row {i} LSE")
+
+
+def pin_prefix_lm(lib):
+    """PrefixLM (Appendix A): keys j < L_p for every row, else j <= i; L_p = 0 and
+    L_p = 1 reduce to causal, L_p >= S to no mask."""
+    S = 13
+    for lp in (0, 1, 4, 12, 13, 20):
+        sets = [set(range(min(lp, S))) | set(range(i + 1)) for i in range(S)]
+        _zero_q_counts(lib, S, sets, f"prefix {lp}", mask=oracle.MASK_PREFIX_LM, prefix_len=lp)
+    B, H, D = 1, 2, 8
+    q, k, v = _rand((B, H, S, D), 42), _rand((B, H, S, D), 43), _rand((B, H, S, D), 44)
+    oc, lc = oracle.attention(q, k, v, scale=0.4, mask=oracle.MASK_CAUSAL, lib=lib)
+    on, ln_ = oracle.attention(q, k, v, scale=0.4, lib=lib)
+    for lp, (oe, le) in ((0, (oc, lc)), (1, (oc, lc)), (S, (on, ln_)), (S + 3, (on, ln_))):
+        op, lp_ = oracle.attention(q, k, v, scale=0.4, mask=oracle.MASK_PREFIX_LM, prefix_len=lp,
+                                   lib=lib)
+        _close(op, oe, 0.0, f"prefix {lp} reduction O")
+        _close(lp_, le, 0.0, f"prefix {lp} reduction LSE")
+
+
+def pin_relative_position(lib):
+    """Score = S + (i - j) (Appendix A). With Q = 0 and V = I the weights of row i
+    are e^(i'-j) / Z_i, Z_i a geometric sum; i' = i + Sk - Sq."""
+    S = 7
+    q = torch.zeros((1, 1, S, S))
+    k = _rand((1, 1, S, S), 45)
+    v = torch.eye(S).reshape(1, 1, S, S)
+    e = math.e
+    o, lse = oracle.attention(q, k, v, scale=1.0, mask=oracle.MASK_CAUSAL, relpos=True, lib=lib)
+    for i in range(S):
+        z = (e ** (i + 1) - 1) / (e - 1)  # sum_{m=0..i} e^m
+        _close(lse[0, 0, i], math.log(z), 1e-12, f"relpos causal Z row {i}")
+        _close(o[0, 0, i], [e ** (i - j) / z if j <= i else 0.0 for j in range(S)], 1e-12,
+               f"relpos causal O row {i}")
+    o, lse = oracle.attention(q, k, v, scale=1.0, relpos=True, lib=lib)
+    for i in range(S):
+        z = sum(e ** (i - j) for j in range(S))
+        _close(lse[0, 0, i], math.log(z), 1e-12, f"relpos Z row {i}")
+    # bottom-right alignment: 3 queries against 7 keys, query i at position i + 4
+    o, lse = oracle.attention(q[:, :, 4:], k, v, scale=1.0, mask=oracle.MASK_CAUSAL,
+                              relpos=True, lib=lib)
+    for i in range(3):
+        ii = i + 4
+        z = (e ** (ii + 1) - 1) / (e - 1)
+        _close(lse[0, 0, i], math.log(z), 1e-12, f"relpos Sq<Sk Z row {i}")
+
+
+def pin_relu_sigmoid(lib):
+    """ReLU(S)/L and Sigmoid(S)/L (Appendix A): with Q = 0 every score is 0, so
+    Sigmoid gives O_i = n_i * mean(V_visible) / (2 L) and ReLU gives O = 0; P rows
+    equal act(S)/L exactly; masked keys get weight 0."""
+    S, D = 9, 4
+    v = _rand((1, 1, S, D), 46)
+    k = _rand((1, 1, S, D), 47)
+    q0 = torch.zeros((1, 1, S, D))
+    vn = v[0, 0].double().numpy()
+    o, lse = oracle.attention(q0, k, v, scale=1.0, mask=oracle.MASK_CAUSAL,
+                              norm=oracle.NORM_SIGMOID, lib=lib)
+    for i in range(S):
+        _close(o[0, 0, i], vn[:i + 1].sum(0) / (2 * S), 1e-12, f"sigmoid Q=0 row {i}")
+    assert np.isnan(lse).all()
+    o, _ = oracle.attention(q0, k, v, scale=1.0, norm=oracle.NORM_RELU, lib=lib)
+    _close(o, np.zeros_like(o), 0.0, "relu Q=0")
+    # P = act(scale * q.k)/L on random scores, against scipy-free closed forms
+    q = _rand((1, 1, S, D), 48, 1.5)
+    s = 0.6 * torch.einsum("bhid,bhjd->bhij", q.double(), k.double()).numpy()
+    for norm, act in ((oracle.NORM_RELU, lambda x: np.maximum(x, 0.0)),
+                      (oracle.NORM_SIGMOID, lambda x: 1.0 / (1.0 + np.exp(-x)))):
+        o, _, p = oracle.attention(q, k, v, scale=0.6, norm=norm, want_probs=True, lib=lib)
+        _close(p, act(s) / S, 1e-12, f"norm {norm} P")
+        o, _, p = oracle.attention(q, k, v, scale=0.6, norm=norm, mask=oracle.MASK_CAUSAL,
+                                   want_probs=True, lib=lib)
+        tri = np.tril(np.ones((S, S), dtype=bool))
+        _close(p[0, 0][~tri], np.zeros((~tri).sum()), 0.0, f"norm {norm} masked P")
+        _close(p[0, 0][tri], (act(s) / S)[0, 0][tri], 1e-12, f"norm {norm} causal P")
+
+
+def pin_global_window(lib):
+    """Global Sliding Window (Appendix A): |i-j| <= w, or i in G, or j in G.
+    G empty reduces to the symmetric sliding window."""
+    S = 14
+    for w, G in ((0, [0]), (2, [0, 1]), (1, [5, 11]), (3, []), (0, list(range(S)))):
+        sets = []
+        for i in range(S):
+            if i in G:
+                sets.append(set(range(S)))
+            else:
+                sets.append({j for j in range(S) if abs(i - j) <= w} | set(G))
+        _zero_q_counts(lib, S, sets, f"global w={w} G={G}", mask=oracle.MASK_GLOBAL_WINDOW,
+                       window_left=w, window_right=w, global_tokens=G)
+    B, H, D = 1, 2, 6
+    q, k, v = _rand((B, H, S, D), 49), _rand((B, H, S, D), 50), _rand((B, H, S, D), 51)
+    ow, lw = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_SLIDING_WINDOW,
+                              window_left=3, window_right=3, lib=lib)
+    og, lg = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_GLOBAL_WINDOW,
+                              window_left=3, window_right=3, global_tokens=[], lib=lib)
+    _close(og, ow, 0.0, "global G=[] O")
+    _close(lg, lw, 0.0, "global G=[] LSE")
+
+
+def _ids_from_starts(S, starts):
+    ids = [-1] * S
+    for k, st in enumerate(starts):
+        for p in range(st, S):
+            ids[p] = k
+    return ids
+
+
+def pin_share_question(lib):
+    """Share Question (Appendix A): a prompt row sees the prompt causally; a row of
+    response A_k sees the prompt and A_k up to itself. No responses is causal."""
+    S = 15
+    for starts in ([4, 7, 12], [0, 5], [3], [1, 2, 3, 4]):
+        ids = _ids_from_starts(S, starts)
+        sets = []
+        for i in range(S):
+            if ids[i] < 0:
+                sets.append(set(range(i + 1)))
+            else:
+                a = starts[ids[i]]
+                sets.append(set(range(starts[0])) | set(range(a, i + 1)))
+        _zero_q_counts(lib, S, sets, f"share question {starts}", mask=oracle.MASK_SHARE_QUESTION,
+                       token_ids=ids)
+    B, H, D = 1, 2, 6
+    q, k, v = _rand((B, H, S, D), 52), _rand((B, H, S, D), 53), _rand((B, H, S, D), 54)
+    oc, lc = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_CAUSAL, lib=lib)
+    os_, ls = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_SHARE_QUESTION,
+                               token_ids=[-1] * S, lib=lib)
+    _close(os_, oc, 0.0, "share question all-prompt O")
+    _close(ls, lc, 0.0, "share question all-prompt LSE")
+
+
+def pin_causal_blockwise(lib):
+    """Causal Blockwise (Appendix A): rows before L_q see their own document up to
+    themselves, test-query rows see every key up to themselves. L_q = 0 or a
+    single document reduce to causal."""
+    S = 16
+    for starts, lq_ in (([0, 3, 8], 12), ([0, 5, 6, 10], 16), ([2, 9], 9), ([0, 4], 0)):
+        ids = _ids_from_starts(S, starts)
+        sets = []
+        for i in range(S):
+            if i >= lq_:
+                sets.append(set(range(i + 1)))
+            else:
+                sets.append({j for j in range(i + 1) if ids[j] == ids[i]})
+        _zero_q_counts(lib, S, sets, f"blockwise {starts} Lq={lq_}",
+                       mask=oracle.MASK_CAUSAL_BLOCKWISE, token_ids=ids, query_start=lq_)
+    B, H, D = 1, 2, 6
+    q, k, v = _rand((B, H, S, D), 55), _rand((B, H, S, D), 56), _rand((B, H, S, D), 57)
+    oc, lc = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_CAUSAL, lib=lib)
+    for ids, lq_ in (([0] * S, S), (_ids_from_starts(S, [0, 7]), 0)):
+        ob, lb = oracle.attention(q, k, v, scale=0.5, mask=oracle.MASK_CAUSAL_BLOCKWISE,
+                                  token_ids=ids, query_start=lq_, lib=lib)
+        _close(ob, oc, 0.0, f"blockwise reduction O (Lq={lq_})")
+        _close(lb, lc, 0.0, f"blockwise reduction LSE (Lq={lq_})")
+
+
 ALL_PINS = [pin_hand_cases, pin_probability_rows, pin_constant_v, pin_causal_row0,
             pin_single_key_window, pin_zero_query_counts, pin_zero_query_alibi,
             pin_reductions, pin_torch_sdpa, pin_gqa_equals_repeated, pin_varlen_concat,
-            pin_varlen_unequal_lengths, pin_row_subset]
+            pin_varlen_unequal_lengths, pin_row_subset, pin_prefix_lm, pin_relative_position,
+            pin_relu_sigmoid, pin_global_window, pin_share_question, pin_causal_blockwise]
 
 
 def failing_pins(lib):

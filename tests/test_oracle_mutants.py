@@ -34,6 +34,28 @@ MUTANTS = [
      "kbase = k + ((int64_t)0 * p->hkv + hk) * p->d;"),
     ("varlen key length from queries", "lk = p->cu_k[b + 1] - p->cu_k[b];", "lk = lq;"),
     ("empty row LSE zero", "lse[row] = -INFINITY;", "lse[row] = 0.0;"),
+    ("prefix inclusive of L_p", "if (j < p->prefix_len) return 1;", "if (j <= p->prefix_len) return 1;"),
+    ("prefix without causal part", "return j <= ii;                  /* causal generation */",
+     "return 0;"),
+    ("relative position sign", "if (p->relpos) s += (double)(i + (lk - lq) - j);",
+     "if (p->relpos) s += (double)(j - i - (lk - lq));"),
+    ("relative position top-left", "if (p->relpos) s += (double)(i + (lk - lq) - j);",
+     "if (p->relpos) s += (double)(i - j);"),
+    ("relative position before soft-cap", "if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);",
+     "if (p->relpos) s += (double)(i + (lk - lq) - j);\n    if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);"),
+    ("norm without 1/L", "double pj = a / (double)lk;", "double pj = a;"),
+    ("ReLU passes negatives", "a = s[j] > 0.0 ? s[j] : 0.0;", "a = s[j];"),
+    ("Sigmoid sign", "a = 1.0 / (1.0 + exp(-s[j]));", "a = 1.0 / (1.0 + exp(s[j]));"),
+    ("global rows not global", "if (in_global(p, ii) || in_global(p, j)) return 1;",
+     "if (in_global(p, j)) return 1;"),
+    ("global keys not global", "if (in_global(p, ii) || in_global(p, j)) return 1;",
+     "if (in_global(p, ii)) return 1;"),
+    ("response blind to prompt", "return idj < 0 || idj == idi;    /* response -> prompt + itself   */",
+     "return idj == idi;"),
+    ("test query starts one late", "if (ii >= p->query_start) return 1;          /* test query visibility   */",
+     "if (ii > p->query_start) return 1;"),
+    ("blockwise across documents", "return p->token_ids[ii] == p->token_ids[j];  /* demonstration isolation */",
+     "return 1;"),
 ]
 
 
