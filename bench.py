@@ -27,40 +27,62 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 import paper_2605_05023_amd as attn  # noqa: E402
-from paper_2605_05023_amd.workloads import WORKLOADS, make_inputs  # noqa: E402
+from paper_2605_05023_amd.workloads import (MASK_CAUSAL, MASK_CAUSAL_BLOCKWISE,  # noqa: E402
+                                            MASK_GLOBAL_WINDOW, MASK_NAMES, MASK_PREFIX_LM,
+                                            MASK_SHARE_QUESTION, MASK_SLIDING_WINDOW, WORKLOADS,
+                                            make_inputs)
 
 METRIC = "attention fwd TFLOP/s (unmasked FLOPs) and % of bf16 MFMA peak, 1 MI355X"
 # Dense bf16 matrix-core peak: 256 CUs x 2.4 GHz x 4096 FLOP/clk/CU (the published 2.5 PFLOP/s).
 PEAK_BF16_TFLOPS = 2516.6
 PEAK_FP32_TFLOPS = 157.3
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2605_05023_amd/csrc/attn_fwd_bf16.hip",
-                  "paper_2605_05023_amd/csrc/attn_fwd_f32.hip",
-                  "paper_2605_05023_amd/csrc/score_mods.h",
-                  "paper_2605_05023_amd/csrc/plan.h",
-                  "paper_2605_05023_amd/csrc/kernel_params.h"]
-MASK_NAMES = {0: "none", 1: "causal", 2: "sliding_window"}
+CSRC = os.path.join(ROOT, "paper_2605_05023_amd", "csrc")
+KERNEL_SOURCES = sorted(os.path.join("paper_2605_05023_amd", "csrc", f) for f in os.listdir(CSRC)
+                        if f.endswith((".hip", ".h")))
+
+
+def row_counts(inp, S: int) -> np.ndarray:
+    """Visible keys of rows 0..S-1 of one sequence of S tokens (Sq == Sk), in
+    closed form per mask kind (Appendix A case analyses)."""
+    wl = inp.wl
+    i = np.arange(S, dtype=np.int64)
+
+    def band(left, right):
+        lo = np.zeros(S, np.int64) if left < 0 else np.maximum(0, i - left)
+        hi = np.full(S, S - 1, np.int64) if right < 0 else np.minimum(S - 1, i + right)
+        return lo, hi
+
+    if wl.mask == MASK_CAUSAL:
+        return i + 1
+    if wl.mask == MASK_SLIDING_WINDOW:
+        lo, hi = band(wl.window_left, wl.window_right)
+        return np.maximum(0, hi - lo + 1)
+    if wl.mask == MASK_PREFIX_LM:  # keys j < L_p, or j <= i
+        return np.maximum(i + 1, min(wl.prefix_len, S))
+    if wl.mask == MASK_GLOBAL_WINDOW:  # |i - j| within the window, or i or j in 0..G-1
+        g = min(wl.num_global, S)
+        lo, hi = band(wl.window_left, wl.window_right)
+        inside = np.maximum(0, hi - lo + 1)
+        overlap = np.maximum(0, np.minimum(hi, g - 1) - lo + 1)  # globals already in the band
+        n = inside + g - overlap
+        return np.where(i < g, S, n)
+    if wl.mask in (MASK_SHARE_QUESTION, MASK_CAUSAL_BLOCKWISE):
+        starts = np.asarray(inp.segment_starts.tolist(), dtype=np.int64)
+        k = np.searchsorted(starts, i, side="right") - 1  # segment of row i, -1 before s_0
+        seg_start = np.where(k >= 0, starts[np.maximum(k, 0)], 0)
+        if wl.mask == MASK_SHARE_QUESTION:  # prompt causal; response: prompt + own segment
+            prompt = min(int(starts[0]), S)
+            return np.where(k < 0, i + 1, prompt + (i - seg_start + 1))
+        return np.where(i >= wl.query_start, i + 1, i - seg_start + 1)
+    return np.full(S, S, np.int64)
 
 
 def visible_pairs(inp) -> int:
-    """Visible (query, key) pairs summed over query heads, in closed form per row:
-    row i sees keys max(0, i - wl) .. min(S - 1, i + wr) of its own sequence."""
+    """Visible (query, key) pairs summed over query heads and sequences."""
     wl = inp.wl
     lengths = inp.lengths if inp.lengths is not None else [wl.seqlen] * wl.batch
-    left = wl.window_left if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW else -1
-    if wl.mask == attn.ATTN_MASK_CAUSAL:
-        right = 0
-    elif wl.mask == attn.ATTN_MASK_SLIDING_WINDOW:
-        right = wl.window_right
-    else:
-        right = -1
-    total = 0
-    for S in lengths:
-        i = np.arange(S, dtype=np.int64)
-        lo = np.zeros(S, np.int64) if left < 0 else np.maximum(0, i - left)
-        hi = np.full(S, S - 1, np.int64) if right < 0 else np.minimum(S - 1, i + right)
-        total += int(np.maximum(0, hi - lo + 1).sum())
-    return total * wl.hq
+    return int(sum(int(row_counts(inp, S).sum()) for S in lengths if S > 0)) * wl.hq
 
 
 def algorithmic_bytes(inp) -> int:
@@ -106,7 +128,8 @@ def cpu_baseline(inp, flops_per_row_fn, min_seconds: float, max_seconds: float, 
     order = rng.permutation(total_rows)
     kw = dict(scale=wl.scale, mask=wl.mask, window_left=wl.window_left,
               window_right=wl.window_right, slopes=inp.slopes, softcap=wl.softcap,
-              cu_seqlens_q=inp.cu_seqlens, cu_seqlens_k=inp.cu_seqlens)
+              cu_seqlens_q=inp.cu_seqlens, cu_seqlens_k=inp.cu_seqlens,
+              **inp.oracle_mask_kwargs())
     oracle.load()
     done, elapsed, flops, batch = 0, 0.0, 0, 256
     while done < total_rows and elapsed < min_seconds:
@@ -135,28 +158,23 @@ def row_flops_fn(inp):
     """Unmasked FLOPs of given flat LSE row ids."""
     wl = inp.wl
     D = wl.head_dim
-    left = wl.window_left if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW else -1
-    right = 0 if wl.mask == attn.ATTN_MASK_CAUSAL else (
-        wl.window_right if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW else -1)
     if inp.cu_seqlens is not None:
         cu = inp.cu_seqlens.numpy().astype(np.int64)
         T = inp.total_tokens
+        counts = [row_counts(inp, int(cu[s + 1] - cu[s])) for s in range(len(cu) - 1)]
 
-        def pos(rows):
+        def per_row(rows):
             t = rows % T
             s = np.searchsorted(cu, t, side="right") - 1
-            return t - cu[s], cu[s + 1] - cu[s]
+            return np.array([counts[a][b] for a, b in zip(s, t - cu[s])], dtype=np.int64)
     else:
-        S = wl.seqlen
+        counts = row_counts(inp, wl.seqlen)
 
-        def pos(rows):
-            return rows % S, np.full(len(rows), S)
+        def per_row(rows):
+            return counts[rows % wl.seqlen]
 
     def fn(rows):
-        i, L = pos(np.asarray(rows, dtype=np.int64))
-        lo = np.zeros_like(i) if left < 0 else np.maximum(0, i - left)
-        hi = L - 1 if right < 0 else np.minimum(L - 1, i + right)
-        return int(4 * D * np.maximum(0, hi - lo + 1).sum())
+        return int(4 * D * per_row(np.asarray(rows, dtype=np.int64)).sum())
     return fn
 
 
@@ -188,23 +206,13 @@ def main():
     out = torch.empty_like(q)
     varlen = inp.cu_seqlens is not None
     lse_shape = (wl.hq, inp.total_tokens) if varlen else (wl.batch, wl.hq, wl.seqlen)
-    lse = torch.empty(lse_shape, dtype=torch.float32, device=dev)
-    slopes = inp.slopes.to(dev) if inp.slopes is not None else None
-    cu = inp.cu_seqlens.to(dev) if varlen else None
-    kw = {}
-    if wl.mask == attn.ATTN_MASK_SLIDING_WINDOW:
-        kw["window"] = (wl.window_left, wl.window_right)
-    else:
-        kw["causal"] = wl.mask == attn.ATTN_MASK_CAUSAL
-    if varlen:
-        kw.update(cu_seqlens_q=cu, cu_seqlens_k=cu, max_seqlen_q=inp.max_seqlen,
-                  max_seqlen_k=inp.max_seqlen)
+    lse = torch.empty(lse_shape, dtype=torch.float32, device=dev) if wl.norm == "softmax" else None
+    vkw = inp.variant_kwargs(dev)  # keeps the device copies of slopes / segments alive
     stream = torch.cuda.current_stream(dev)
-    desc = attn.make_desc(q, k, v, out, alibi_slopes=slopes, softcap=wl.softcap, scale=wl.scale,
-                          stream=stream.cuda_stream, **kw)
+    desc = attn.make_desc(q, k, v, out, stream=stream.cuda_stream, **vkw)
     lib = attn.load()
-    args_c = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
-              ctypes.byref(desc))
+    args_c = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+              lse.data_ptr() if lse is not None else None, ctypes.byref(desc))
 
     def step():
         rc = lib.attn_fwd(*args_c)
@@ -262,9 +270,16 @@ def main():
             "seqlen": wl.seqlen if not varlen else f"varlen, total {inp.total_tokens}",
             "head_dim": wl.head_dim,
             "mask": MASK_NAMES[wl.mask],
-            "window": [wl.window_left, wl.window_right] if wl.mask == 2 else None,
+            "window": [wl.window_left, wl.window_right]
+            if wl.mask in (MASK_SLIDING_WINDOW, MASK_GLOBAL_WINDOW) else None,
             "alibi": wl.alibi,
             "softcap": wl.softcap,
+            "relative_position": wl.relpos,
+            "norm": wl.norm,
+            "prefix_len": wl.prefix_len if wl.mask in (MASK_PREFIX_LM, MASK_SHARE_QUESTION) else None,
+            "num_global": wl.num_global if wl.mask == MASK_GLOBAL_WINDOW else None,
+            "segment_starts": inp.segment_starts.tolist() if inp.segment_starts is not None else None,
+            "query_start": wl.query_start if wl.mask == MASK_CAUSAL_BLOCKWISE else None,
             "unmasked_flops_per_step": flops,
         },
         "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),

@@ -2,20 +2,25 @@
  * attn.h -- C ABI of the gfx950 fused attention forward library (libattn.so).
  *
  * The library computes the forward pass of scaled-dot-product attention,
- * O = Softmax(Score(scale * Q K^T) + Mask) V (Eq. 1 of Section 2.2 and the
- * Score / Mask / Norm decomposition of Eq. 2 and Appendix A), together with
- * the natural-log row normaliser LSE_i = log sum_j exp(score_ij). It runs as
- * one fused, tiled kernel with an online softmax on an AMD Instinct MI355X
- * (gfx950). Every argument is a plain pointer or integer; no C++ or framework
- * type crosses this boundary.
+ * O = Norm(Mask(Score(scale * Q K^T))) V (Eq. 1 of Section 2.2 and the
+ * Score / Mask / Norm decomposition of Eq. 2 and Appendix A). With the
+ * softmax normalisation it also returns the natural-log row normaliser
+ * LSE_i = log sum_j exp(score_ij). It runs as one fused, tiled kernel (an
+ * online softmax for Norm = softmax) on an AMD Instinct MI355X (gfx950).
+ * Every argument is a plain pointer or integer; no C++ or framework type
+ * crosses this boundary.
  *
  * Variants carried by attn_variant_desc (Appendix A; Appendix C names the
  * first four as the expert-library built-ins):
  *   - causal mask, sliding-window mask, ALiBi bias, tanh soft-cap
  *     (Appendix A "Softcap Attention": C * tanh(S / C)),
  *   - grouped-query heads (Section 4.1 workload tuples, e.g. 64/8/128),
- *   - variable-length packed batches (cu_seqlens prefix sums).
- * Order inside the score: scale, then soft-cap, then ALiBi bias, then mask.
+ *   - variable-length packed batches (cu_seqlens prefix sums),
+ *   - the PrefixLM, Global Sliding Window, Share Question and Causal
+ *     Blockwise masks, the relative-position score term (i - j), and the
+ *     ReLU and Sigmoid normalisations of Appendix A.
+ * Order inside the score: scale, then soft-cap, then the ALiBi and relative
+ * position biases, then the mask, then the normalisation.
  *
  * Ownership: the caller allocates and owns every buffer. The library never
  * allocates, frees or keeps a user pointer beyond the enqueued kernel. All
@@ -38,7 +43,10 @@
 extern "C" {
 #endif
 
-#define ATTN_ABI_VERSION 1
+#define ATTN_ABI_VERSION 2
+
+/* Largest attn_variant_desc.num_segments (segments are staged on chip). */
+#define ATTN_MAX_SEGMENTS 2048
 
 typedef enum attn_dtype {
     ATTN_BF16 = 0, /* q, k, v, out are bfloat16; accumulation in fp32 */
@@ -54,19 +62,55 @@ typedef enum attn_dtype {
  *   SLIDING_WINDOW : i' - j <= window_left and j - i' <= window_right, where
  *                    a negative bound is unbounded. (1023, 0) keeps keys
  *                    i'-1023 .. i'; (-1, 0) is CAUSAL; (-1, -1) is NONE.
- * A row with no visible key gets O = 0 and LSE = -inf.
+ *   PREFIX_LM      : j < prefix_len, or j <= i' (Appendix A "PrefixLM": the
+ *                    prefix of length L_p is keys 0 .. L_p-1, 0-based).
+ *   GLOBAL_SLIDING_WINDOW : i' - j <= window_left and j - i' <= window_right
+ *                    (the paper's |i - j| <= w is window_left = window_right
+ *                    = w), or i' in G, or j in G, where the global set G is
+ *                    positions 0 .. num_global-1 (Appendix A "Global Sliding
+ *                    Window").
+ *   SHARE_QUESTION : positions before segment_starts[0] are the prompt Q;
+ *                    segment k (positions segment_starts[k] up to the next
+ *                    start, the last one up to the end) is response A_k.
+ *                    Visible iff j <= i' and either both are in Q, or i' is
+ *                    in A_k and j is in Q or A_k (Appendix A "Share Question
+ *                    Mask").
+ *   CAUSAL_BLOCKWISE : segment k is document k (positions before
+ *                    segment_starts[0] form one more document). Visible iff
+ *                    j <= i' and either i' >= query_start or i' and j lie in
+ *                    the same document (Appendix A "Causal Blockwise Mask").
+ * A row with no visible key gets O = 0 and (softmax) LSE = -inf.
  */
 typedef enum attn_mask_kind {
     ATTN_MASK_NONE = 0,
     ATTN_MASK_CAUSAL = 1,
-    ATTN_MASK_SLIDING_WINDOW = 2
+    ATTN_MASK_SLIDING_WINDOW = 2,
+    ATTN_MASK_PREFIX_LM = 3,
+    ATTN_MASK_GLOBAL_SLIDING_WINDOW = 4,
+    ATTN_MASK_SHARE_QUESTION = 5,
+    ATTN_MASK_CAUSAL_BLOCKWISE = 6
 } attn_mask_kind_t;
+
+/*
+ * Norm stage (Eq. 2 and Appendix A "Normalization Variants"), with
+ * L = the key length of the row's sequence (seqlen_k, or its varlen length):
+ *   SOFTMAX : P_ij = exp(s_ij) / sum_j exp(s_ij); lse is written.
+ *   RELU    : P_ij = ReLU(s_ij) / L; lse is not written.
+ *   SIGMOID : P_ij = Sigmoid(s_ij) / L; lse is not written.
+ * Masked scores are -inf, which every normalisation sends to P = 0.
+ */
+typedef enum attn_norm_kind {
+    ATTN_NORM_SOFTMAX = 0,
+    ATTN_NORM_RELU = 1,
+    ATTN_NORM_SIGMOID = 2
+} attn_norm_kind_t;
 
 typedef enum attn_status {
     ATTN_OK = 0,
     ATTN_ERR_NULL_PTR = -1,    /* a required pointer is NULL                   */
     ATTN_ERR_BAD_SHAPE = -2,   /* non-positive or inconsistent sizes/strides    */
-    ATTN_ERR_BAD_VARIANT = -3, /* unknown mask kind, bad window or soft-cap     */
+    ATTN_ERR_BAD_VARIANT = -3, /* unknown mask or norm kind, or a bad window,
+                                  soft-cap, prefix or segment count            */
     ATTN_ERR_ALIGNMENT = -4,   /* base not 16-byte aligned, stride not multiple
                                   of 16 bytes, or head-dim stride not 1          */
     ATTN_ERR_UNSUPPORTED = -5, /* head_dim or dtype outside the compiled set    */
@@ -119,13 +163,25 @@ typedef struct attn_variant_desc {
     int64_t stride_v_b, stride_v_h, stride_v_s;
     int64_t stride_o_b, stride_o_h, stride_o_s;
     void *stream;                /* hipStream_t to enqueue on; NULL = default      */
+    int32_t norm_kind;           /* attn_norm_kind_t                               */
+    int32_t relative_position;   /* 1: add (i' - j) to the score after the
+                                    soft-cap (Appendix A "Relative Position
+                                    Embeddings"); 0: off                           */
+    int32_t prefix_len;          /* PREFIX_LM: L_p >= 0                             */
+    int32_t num_global;          /* GLOBAL_SLIDING_WINDOW: size of G >= 0          */
+    const int32_t *segment_starts; /* SHARE_QUESTION, CAUSAL_BLOCKWISE: device
+                                    int32 [num_segments], strictly increasing,
+                                    >= 0; positions are per sequence (varlen)     */
+    int32_t num_segments;        /* 1 .. ATTN_MAX_SEGMENTS for those kinds         */
+    int32_t query_start;         /* CAUSAL_BLOCKWISE: L_q >= 0                      */
 } attn_variant_desc;
 
 /*
  * Enqueue the attention forward pass on desc->stream.
  *   q, k, v : device inputs (layouts above), read only
  *   out     : device output, same dtype and layout as q; may not alias inputs
- *   lse     : device fp32 output (layout above), or NULL to skip it
+ *   lse     : device fp32 output (layout above), or NULL to skip it; only
+ *             written for the softmax normalisation
  * Returns ATTN_OK once the kernel is enqueued (it runs asynchronously), or an
  * error code; on error nothing was enqueued. A zero-sized problem (batch,
  * seqlen or total of 0) enqueues nothing and returns ATTN_OK.
@@ -149,11 +205,26 @@ int attn_abi_version(void);
  * Tiles in [out[0], out[1]) and [out[2], out[3]) need the element mask; tiles
  * in [out[1], out[2]) are fully visible for every row; tiles outside
  * [out[0], out[3]) are fully masked and skipped (loop splitting, Section 3.4).
- * When no tile is touched out[0] == out[3]. Only mask_kind, window_left and
- * window_right of desc are read.
+ * When no tile is touched out[0] == out[3]. Only mask_kind, window_left,
+ * window_right and prefix_len of desc are read. The kinds whose pattern comes
+ * from per-position data (GLOBAL_SLIDING_WINDOW, SHARE_QUESTION,
+ * CAUSAL_BLOCKWISE) are planned inside the kernel from the rows' visible
+ * ranges and return ATTN_ERR_UNSUPPORTED here.
  */
 int attn_plan_tiles(const attn_variant_desc *desc, int32_t q0, int32_t rows, int32_t lq,
                     int32_t lk, int32_t block_n, int32_t out[4]);
+
+/*
+ * Keys visible to query row i (0 <= i < lq) of a sequence with lk keys under
+ * the mask of `desc` (host mirror of the kernels' per-row visibility, exposed
+ * so the masks can be tested without a GPU): keys j < out[0] and keys
+ * out[1] <= j <= out[2] (empty when out[1] > out[2]). segment_starts is a
+ * HOST copy of desc->segment_starts (read only for SHARE_QUESTION and
+ * CAUSAL_BLOCKWISE); desc->segment_starts itself is not read. Reads the mask
+ * fields of desc only.
+ */
+int attn_row_range(const attn_variant_desc *desc, const int32_t *segment_starts, int32_t i,
+                   int32_t lq, int32_t lk, int32_t out[3]);
 
 #ifdef __cplusplus
 }

@@ -13,20 +13,38 @@ from typing import Optional
 
 import torch
 
-from ._abi import (ATTN_BF16, ATTN_FP32, ATTN_MASK_CAUSAL, ATTN_MASK_NONE,  # noqa: F401
-                   ATTN_MASK_SLIDING_WINDOW, AttnError, AttnVariantDesc, check, load, plan_tiles)
+from ._abi import (ATTN_BF16, ATTN_FP32, ATTN_MASK_CAUSAL, ATTN_MASK_CAUSAL_BLOCKWISE,  # noqa: F401
+                   ATTN_MASK_GLOBAL_SLIDING_WINDOW, ATTN_MASK_NONE, ATTN_MASK_PREFIX_LM,
+                   ATTN_MASK_SHARE_QUESTION, ATTN_MASK_SLIDING_WINDOW, ATTN_NORM_RELU,
+                   ATTN_NORM_SIGMOID, ATTN_NORM_SOFTMAX, AttnError, AttnVariantDesc, check, load,
+                   plan_tiles, row_range)
 
-__all__ = ["fwd", "make_desc", "AttnError", "AttnVariantDesc", "load", "plan_tiles",
+__all__ = ["fwd", "make_desc", "AttnError", "AttnVariantDesc", "load", "plan_tiles", "row_range",
            "ATTN_BF16", "ATTN_FP32", "ATTN_MASK_NONE", "ATTN_MASK_CAUSAL",
-           "ATTN_MASK_SLIDING_WINDOW"]
+           "ATTN_MASK_SLIDING_WINDOW", "ATTN_MASK_PREFIX_LM", "ATTN_MASK_GLOBAL_SLIDING_WINDOW",
+           "ATTN_MASK_SHARE_QUESTION", "ATTN_MASK_CAUSAL_BLOCKWISE", "ATTN_NORM_SOFTMAX",
+           "ATTN_NORM_RELU", "ATTN_NORM_SIGMOID"]
 
 _DTYPES = {torch.bfloat16: ATTN_BF16, torch.float32: ATTN_FP32}
+_MASKS = {"none": ATTN_MASK_NONE, "causal": ATTN_MASK_CAUSAL,
+          "sliding_window": ATTN_MASK_SLIDING_WINDOW, "prefix_lm": ATTN_MASK_PREFIX_LM,
+          "global_sliding_window": ATTN_MASK_GLOBAL_SLIDING_WINDOW,
+          "share_question": ATTN_MASK_SHARE_QUESTION,
+          "causal_blockwise": ATTN_MASK_CAUSAL_BLOCKWISE}
+_NORMS = {"softmax": ATTN_NORM_SOFTMAX, "relu": ATTN_NORM_RELU, "sigmoid": ATTN_NORM_SIGMOID}
 
 
 def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, softcap=0.0,
               scale=None, cu_seqlens_q=None, cu_seqlens_k=None, max_seqlen_q=None,
-              max_seqlen_k=None, stream=None) -> AttnVariantDesc:
-    """Build the descriptor for tensors q/k/v/out (see include/attn.h for layouts)."""
+              max_seqlen_k=None, stream=None, mask=None, prefix_len=0, num_global=0,
+              segment_starts=None, query_start=0, relative_position=False,
+              norm="softmax") -> AttnVariantDesc:
+    """Build the descriptor for tensors q/k/v/out (see include/attn.h for layouts).
+
+    `mask` names any attn_mask_kind_t ("prefix_lm", "global_sliding_window",
+    "share_question", "causal_blockwise", ...) and overrides causal/window;
+    `window` gives the (left, right) bounds of the two window masks.
+    """
     if q.dtype not in _DTYPES or k.dtype != q.dtype or v.dtype != q.dtype or out.dtype != q.dtype:
         raise TypeError("q, k, v, out must share dtype bfloat16 or float32")
     d = AttnVariantDesc.new()
@@ -35,11 +53,25 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
     D = q.shape[-1]
     d.head_dim = D
     d.scale = float(scale) if scale is not None else 1.0 / math.sqrt(D)
-    if window is not None:
+    if mask is not None:
+        d.mask_kind = _MASKS[mask] if isinstance(mask, str) else int(mask)
+    elif window is not None:
         d.mask_kind = ATTN_MASK_SLIDING_WINDOW
-        d.window_left, d.window_right = int(window[0]), int(window[1])
     else:
         d.mask_kind = ATTN_MASK_CAUSAL if causal else ATTN_MASK_NONE
+    if window is not None:
+        d.window_left, d.window_right = int(window[0]), int(window[1])
+    else:
+        d.window_left = d.window_right = -1
+    d.prefix_len, d.num_global, d.query_start = int(prefix_len), int(num_global), int(query_start)
+    d.relative_position = 1 if relative_position else 0
+    d.norm_kind = _NORMS[norm] if isinstance(norm, str) else int(norm)
+    if segment_starts is not None:
+        if (segment_starts.dtype != torch.int32 or segment_starts.device != q.device
+                or not segment_starts.is_contiguous()):
+            raise TypeError("segment_starts must be contiguous int32 on q's device")
+        d.segment_starts = segment_starts.data_ptr()
+        d.num_segments = segment_starts.numel()
     d.softcap = float(softcap)
     if alibi_slopes is not None:
         if alibi_slopes.dtype != torch.float32 or alibi_slopes.device != q.device:
@@ -80,12 +112,17 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
 
 def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softcap: float = 0.0,
         scale: Optional[float] = None, cu_seqlens_q=None, cu_seqlens_k=None, max_seqlen_q=None,
-        max_seqlen_k=None, out=None, lse=None, return_lse: bool = True):
+        max_seqlen_k=None, out=None, lse=None, return_lse: bool = True, mask=None,
+        prefix_len: int = 0, num_global: int = 0, segment_starts=None, query_start: int = 0,
+        relative_position: bool = False, norm="softmax"):
     """Attention forward on the GPU.
 
     Fixed length: q [B,Hq,S,D], k/v [B,Hkv,Sk,D] -> out like q, lse [B,Hq,S] fp32.
     Varlen: q [Tq,Hq,D], k/v [Tk,Hkv,D], cu_seqlens int32 [B+1] -> lse [Hq,Tq].
     window=(left, right) selects the sliding-window mask (-1 = unbounded).
+    The other variants of include/attn.h are selected by `mask` (with
+    prefix_len, num_global, segment_starts, query_start), `relative_position`
+    and `norm` ("softmax", "relu", "sigmoid"; only softmax produces an LSE).
     """
     if not q.is_cuda:
         raise ValueError("fwd runs on the GPU only; q, k, v must be device tensors")
@@ -93,6 +130,9 @@ def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softca
     varlen = cu_seqlens_q is not None
     if out is None:
         out = torch.empty_like(q)
+    softmax = (_NORMS[norm] if isinstance(norm, str) else int(norm)) == ATTN_NORM_SOFTMAX
+    if not softmax:
+        return_lse, lse = False, None
     if lse is None and return_lse:
         shape = (q.shape[1], q.shape[0]) if varlen else (q.shape[0], q.shape[1], q.shape[2])
         lse = torch.empty(shape, dtype=torch.float32, device=q.device)
@@ -101,7 +141,9 @@ def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softca
     d = make_desc(q, k, v, out, causal=causal, window=window, alibi_slopes=alibi_slopes,
                   softcap=softcap, scale=scale, cu_seqlens_q=cu_seqlens_q,
                   cu_seqlens_k=cu_seqlens_k, max_seqlen_q=max_seqlen_q,
-                  max_seqlen_k=max_seqlen_k)
+                  max_seqlen_k=max_seqlen_k, mask=mask, prefix_len=prefix_len,
+                  num_global=num_global, segment_starts=segment_starts, query_start=query_start,
+                  relative_position=relative_position, norm=norm)
     status = lib.attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                           lse.data_ptr() if lse is not None else None, ctypes.byref(d))
     check(status, lib)

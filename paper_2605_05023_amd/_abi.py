@@ -12,9 +12,13 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libattn.so")
 
-ATTN_ABI_VERSION = 1
+ATTN_ABI_VERSION = 2
+ATTN_MAX_SEGMENTS = 2048
 ATTN_BF16, ATTN_FP32 = 0, 1
 ATTN_MASK_NONE, ATTN_MASK_CAUSAL, ATTN_MASK_SLIDING_WINDOW = 0, 1, 2
+ATTN_MASK_PREFIX_LM, ATTN_MASK_GLOBAL_SLIDING_WINDOW = 3, 4
+ATTN_MASK_SHARE_QUESTION, ATTN_MASK_CAUSAL_BLOCKWISE = 5, 6
+ATTN_NORM_SOFTMAX, ATTN_NORM_RELU, ATTN_NORM_SIGMOID = 0, 1, 2
 
 STATUS = {
     0: "ATTN_OK",
@@ -28,7 +32,8 @@ STATUS = {
 }
 STATUS_CODE = {v: k for k, v in STATUS.items()}
 
-EXPORTED = ("attn_fwd", "attn_status_string", "attn_abi_version", "attn_plan_tiles")
+EXPORTED = ("attn_fwd", "attn_status_string", "attn_abi_version", "attn_plan_tiles",
+            "attn_row_range")
 
 
 class AttnVariantDesc(ctypes.Structure):
@@ -58,6 +63,13 @@ class AttnVariantDesc(ctypes.Structure):
         ("stride_v_b", ctypes.c_int64), ("stride_v_h", ctypes.c_int64), ("stride_v_s", ctypes.c_int64),
         ("stride_o_b", ctypes.c_int64), ("stride_o_h", ctypes.c_int64), ("stride_o_s", ctypes.c_int64),
         ("stream", ctypes.c_void_p),
+        ("norm_kind", ctypes.c_int32),
+        ("relative_position", ctypes.c_int32),
+        ("prefix_len", ctypes.c_int32),
+        ("num_global", ctypes.c_int32),
+        ("segment_starts", ctypes.c_void_p),
+        ("num_segments", ctypes.c_int32),
+        ("query_start", ctypes.c_int32),
     ]
 
     @classmethod
@@ -95,6 +107,10 @@ def load(path: str = LIB_PATH):
     lib.attn_plan_tiles.argtypes = [ctypes.POINTER(AttnVariantDesc), ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                     ctypes.POINTER(ctypes.c_int32)]
+    lib.attn_row_range.restype = ctypes.c_int
+    lib.attn_row_range.argtypes = [ctypes.POINTER(AttnVariantDesc), ctypes.POINTER(ctypes.c_int32),
+                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.POINTER(ctypes.c_int32)]
     if lib.attn_abi_version() != ATTN_ABI_VERSION:
         raise ImportError("libattn.so ABI version mismatch")
     if path == LIB_PATH:
@@ -109,12 +125,25 @@ def check(status: int, lib=None) -> None:
 
 
 def plan_tiles(mask_kind: int, window_left: int, window_right: int, q0: int, rows: int, lq: int,
-               lk: int, block_n: int, lib=None):
+               lk: int, block_n: int, lib=None, prefix_len: int = 0):
     """Host mirror of the in-kernel tile planner: (lo, full_lo, full_hi, hi)."""
     lib = lib or load()
     d = AttnVariantDesc.new()
     d.mask_kind, d.window_left, d.window_right = mask_kind, window_left, window_right
+    d.prefix_len = prefix_len
     d.scale = 1.0
     out = (ctypes.c_int32 * 4)()
     check(lib.attn_plan_tiles(ctypes.byref(d), q0, rows, lq, lk, block_n, out), lib)
+    return tuple(out)
+
+
+def row_range(desc: AttnVariantDesc, i: int, lq: int, lk: int, segment_starts=None, lib=None):
+    """Host mirror of the kernels' per-row visibility: (pfx, jlo, jhi), keys
+    j < pfx and jlo <= j <= jhi are visible. `segment_starts`: host ints."""
+    lib = lib or load()
+    seg = None
+    if segment_starts is not None:
+        seg = (ctypes.c_int32 * max(1, len(segment_starts)))(*segment_starts)
+    out = (ctypes.c_int32 * 3)()
+    check(lib.attn_row_range(ctypes.byref(desc), seg, i, lq, lk, out), lib)
     return tuple(out)

@@ -11,6 +11,7 @@
 #include "../../include/attn.h"
 #include "kernel_params.h"
 #include "launch.h"
+#include "row_vis.h"
 
 namespace {
 
@@ -61,7 +62,7 @@ extern "C" const char* attn_status_string(int status)
     case ATTN_OK: return "ok";
     case ATTN_ERR_NULL_PTR: return "a required pointer is NULL";
     case ATTN_ERR_BAD_SHAPE: return "non-positive or inconsistent sizes or strides";
-    case ATTN_ERR_BAD_VARIANT: return "bad mask kind, window, scale or soft-cap";
+    case ATTN_ERR_BAD_VARIANT: return "bad mask or norm kind, window, scale, soft-cap, prefix or segments";
     case ATTN_ERR_ALIGNMENT: return "pointer or stride not 16-byte aligned";
     case ATTN_ERR_UNSUPPORTED: return "head_dim, dtype or size outside the compiled set";
     case ATTN_ERR_ABI: return "attn_variant_desc.struct_size does not match the library";
@@ -70,28 +71,55 @@ extern "C" const char* attn_status_string(int status)
     }
 }
 
+// The band (plan.h) of the closed-form mask kinds; for the global sliding
+// window it is the window part.
 static KeyBand band_of(const attn_variant_desc* d)
 {
-    KeyBand b;
-    if (d->mask_kind == ATTN_MASK_CAUSAL) {
-        b.wl = -1;
+    KeyBand b = {-1, -1, 0};
+    switch (d->mask_kind) {
+    case ATTN_MASK_CAUSAL: b.wr = 0; break;
+    case ATTN_MASK_PREFIX_LM:
         b.wr = 0;
-    } else if (d->mask_kind == ATTN_MASK_SLIDING_WINDOW) {
+        b.pl = d->prefix_len;
+        break;
+    case ATTN_MASK_SLIDING_WINDOW:
+    case ATTN_MASK_GLOBAL_SLIDING_WINDOW:
         b.wl = d->window_left < 0 ? -1 : d->window_left;
         b.wr = d->window_right < 0 ? -1 : d->window_right;
-    } else {
-        b.wl = -1;
-        b.wr = -1;
+        break;
+    default: break;
     }
     return b;
 }
 
+static bool closed_form_mask(int kind)
+{
+    return kind == ATTN_MASK_NONE || kind == ATTN_MASK_CAUSAL ||
+           kind == ATTN_MASK_SLIDING_WINDOW || kind == ATTN_MASK_PREFIX_LM;
+}
+
+static bool segment_mask(int kind)
+{
+    return kind == ATTN_MASK_SHARE_QUESTION || kind == ATTN_MASK_CAUSAL_BLOCKWISE;
+}
+
 static int check_variant(const attn_variant_desc* d)
 {
-    if (d->mask_kind < ATTN_MASK_NONE || d->mask_kind > ATTN_MASK_SLIDING_WINDOW)
+    if (d->mask_kind < ATTN_MASK_NONE || d->mask_kind > ATTN_MASK_CAUSAL_BLOCKWISE)
         return ATTN_ERR_BAD_VARIANT;
-    if (d->mask_kind == ATTN_MASK_SLIDING_WINDOW && (d->window_left < -1 || d->window_right < -1))
+    if ((d->mask_kind == ATTN_MASK_SLIDING_WINDOW ||
+         d->mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW) &&
+        (d->window_left < -1 || d->window_right < -1))
         return ATTN_ERR_BAD_VARIANT;
+    if (d->mask_kind == ATTN_MASK_PREFIX_LM && d->prefix_len < 0) return ATTN_ERR_BAD_VARIANT;
+    if (d->mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d->num_global < 0)
+        return ATTN_ERR_BAD_VARIANT;
+    if (segment_mask(d->mask_kind) &&
+        (d->num_segments < 1 || d->num_segments > ATTN_MAX_SEGMENTS || d->query_start < 0))
+        return ATTN_ERR_BAD_VARIANT;
+    if (d->norm_kind < ATTN_NORM_SOFTMAX || d->norm_kind > ATTN_NORM_SIGMOID)
+        return ATTN_ERR_BAD_VARIANT;
+    if (d->relative_position != 0 && d->relative_position != 1) return ATTN_ERR_BAD_VARIANT;
     if (!std::isfinite(d->scale) || !(d->scale > 0.0f)) return ATTN_ERR_BAD_VARIANT;
     if (!std::isfinite(d->softcap) || d->softcap < 0.0f) return ATTN_ERR_BAD_VARIANT;
     return ATTN_OK;
@@ -104,12 +132,32 @@ extern "C" int attn_plan_tiles(const attn_variant_desc* desc, int32_t q0, int32_
     if (desc->struct_size != sizeof(attn_variant_desc)) return ATTN_ERR_ABI;
     int rc = check_variant(desc);
     if (rc != ATTN_OK) return rc;
+    if (!closed_form_mask(desc->mask_kind)) return ATTN_ERR_UNSUPPORTED;
     if (block_n <= 0 || lq < 0 || lk < 0 || rows < 0 || q0 < 0) return ATTN_ERR_BAD_SHAPE;
     TilePlan p = plan_tiles(band_of(desc), q0, rows, lq, lk, block_n);
     out[0] = p.lo;
     out[1] = p.full_lo;
     out[2] = p.full_hi;
     out[3] = p.hi;
+    return ATTN_OK;
+}
+
+extern "C" int attn_row_range(const attn_variant_desc* desc, const int32_t* segment_starts,
+                              int32_t i, int32_t lq, int32_t lk, int32_t out[3])
+{
+    if (!desc || !out) return ATTN_ERR_NULL_PTR;
+    if (desc->struct_size != sizeof(attn_variant_desc)) return ATTN_ERR_ABI;
+    int rc = check_variant(desc);
+    if (rc != ATTN_OK) return rc;
+    if (segment_mask(desc->mask_kind) && !segment_starts) return ATTN_ERR_NULL_PTR;
+    if (i < 0 || i >= lq || lk < 0) return ATTN_ERR_BAD_SHAPE;
+    const int32_t* seg = segment_mask(desc->mask_kind) ? segment_starts : nullptr;
+    const int32_t nseg = seg ? desc->num_segments : 0;
+    RowVis r = row_visibility(desc->mask_kind, band_of(desc), desc->num_global, seg, nseg,
+                              desc->query_start, i, lq, lk);
+    out[0] = r.pfx;
+    out[1] = r.jlo;
+    out[2] = r.jhi;
     return ATTN_OK;
 }
 
@@ -168,6 +216,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     if (blocks == 0) return ATTN_OK;  // nothing to compute
 
     if (!q || !k || !v || !out) return ATTN_ERR_NULL_PTR;
+    if (segment_mask(d.mask_kind) && !d.segment_starts) return ATTN_ERR_NULL_PTR;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
         return ATTN_ERR_ALIGNMENT;
     if ((reinterpret_cast<uintptr_t>(lse) & 3u) != 0) return ATTN_ERR_ALIGNMENT;
@@ -189,11 +238,20 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.num_q_tiles = (int32_t)q_tiles;
     p.total_q = varlen ? d.total_q : 0;
     p.band = band_of(&d);
+    p.mask_kind = d.mask_kind;
+    p.num_global = d.num_global;
+    p.seg = segment_mask(d.mask_kind) ? d.segment_starts : nullptr;
+    p.num_seg = segment_mask(d.mask_kind) ? d.num_segments : 0;
+    p.query_start = d.query_start;
+    p.norm = d.norm_kind;
+    p.relpos = d.relative_position;
+    // softmax runs in base 2; the other normalisations need natural scores
+    p.unit = d.norm_kind == ATTN_NORM_SOFTMAX ? 1.4426950408889634f : 1.0f;
     p.scale = d.scale;
-    p.scale_log2 = d.scale * 1.4426950408889634f;
+    p.scale_u = d.scale * p.unit;
     p.softcap = d.softcap;
     p.softcap_pre = d.softcap > 0.0f ? d.scale / d.softcap : 0.0f;
-    p.softcap_post = d.softcap * 1.4426950408889634f;
+    p.softcap_post_u = d.softcap * p.unit;
     // Keep each kv-head group on one XCD when the groups divide evenly.
     p.map_mode = ((int64_t)d.batch * d.num_kv_heads) % 8 == 0 ? 1 : 0;
     if (const char* env = std::getenv("ATTN_MAP_MODE")) {

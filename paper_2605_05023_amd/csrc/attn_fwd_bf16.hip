@@ -1,0 +1,47 @@
+// attn_fwd_bf16.hip -- bf16 dispatcher and the head-dim-128 instantiations of
+// the closed-form-mask softmax kernels (none, causal, sliding window,
+// PrefixLM, with soft-cap and one of ALiBi or the relative position bias).
+// Everything else runs the general-path instantiations of the
+// attn_fwd_bf16_general_*.hip units.
+#include "bf16_kernel.h"
+
+namespace attn {
+
+int bf16_block_m() { return BM; }
+
+namespace {
+
+template <int D>
+hipError_t launch_closed_form(const AttnParams& p, hipStream_t stream)
+{
+    const bool sc = p.softcap > 0.0f;
+    const int bias = p.slopes ? kBiasAlibi : (p.relpos ? kBiasRelPos : kBiasNone);
+    if (sc) {
+        if (bias == kBiasAlibi) return launch_variant<D, true, kBiasAlibi, kNormSoftmax, false>(p, stream);
+        if (bias == kBiasRelPos) return launch_variant<D, true, kBiasRelPos, kNormSoftmax, false>(p, stream);
+        return launch_variant<D, true, kBiasNone, kNormSoftmax, false>(p, stream);
+    }
+    if (bias == kBiasAlibi) return launch_variant<D, false, kBiasAlibi, kNormSoftmax, false>(p, stream);
+    if (bias == kBiasRelPos) return launch_variant<D, false, kBiasRelPos, kNormSoftmax, false>(p, stream);
+    return launch_variant<D, false, kBiasNone, kNormSoftmax, false>(p, stream);
+}
+
+}  // namespace
+
+hipError_t launch_bf16_closed_form_d128(const AttnParams& p, hipStream_t stream)
+{
+    return launch_closed_form<128>(p, stream);
+}
+
+hipError_t launch_bf16(const AttnParams& p, int head_dim, hipStream_t stream)
+{
+    const bool closed = p.mask_kind >= 0 && p.mask_kind <= 3;  // band masks of plan.h
+    const bool both_biases = p.slopes != nullptr && p.relpos != 0;
+    if (p.norm == kNormRelu) return launch_bf16_general_relu(p, head_dim, stream);
+    if (p.norm == kNormSigmoid) return launch_bf16_general_sigmoid(p, head_dim, stream);
+    if (!closed || both_biases) return launch_bf16_general_softmax(p, head_dim, stream);
+    if (head_dim == 128) return launch_bf16_closed_form_d128(p, stream);
+    return launch_bf16_closed_form_d64(p, stream);
+}
+
+}  // namespace attn

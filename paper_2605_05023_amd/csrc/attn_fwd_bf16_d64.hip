@@ -1,0 +1,21 @@
+// attn_fwd_bf16_d64.hip -- head-dim-64 instantiations of the closed-form-mask
+// softmax kernels (see attn_fwd_bf16.hip).
+#include "bf16_kernel.h"
+
+namespace attn {
+
+hipError_t launch_bf16_closed_form_d64(const AttnParams& p, hipStream_t stream)
+{
+    const bool sc = p.softcap > 0.0f;
+    const int bias = p.slopes ? kBiasAlibi : (p.relpos ? kBiasRelPos : kBiasNone);
+    if (sc) {
+        if (bias == kBiasAlibi) return launch_variant<64, true, kBiasAlibi, kNormSoftmax, false>(p, stream);
+        if (bias == kBiasRelPos) return launch_variant<64, true, kBiasRelPos, kNormSoftmax, false>(p, stream);
+        return launch_variant<64, true, kBiasNone, kNormSoftmax, false>(p, stream);
+    }
+    if (bias == kBiasAlibi) return launch_variant<64, false, kBiasAlibi, kNormSoftmax, false>(p, stream);
+    if (bias == kBiasRelPos) return launch_variant<64, false, kBiasRelPos, kNormSoftmax, false>(p, stream);
+    return launch_variant<64, false, kBiasNone, kNormSoftmax, false>(p, stream);
+}
+
+}  // namespace attn

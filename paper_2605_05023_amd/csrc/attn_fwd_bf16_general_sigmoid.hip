@@ -1,0 +1,12 @@
+// attn_fwd_bf16_general_sigmoid.hip -- general-path bf16 kernels (per-row visible
+// ranges, runtime-coefficient bias) with the sigmoid normalisation.
+#include "bf16_kernel.h"
+
+namespace attn {
+
+hipError_t launch_bf16_general_sigmoid(const AttnParams& p, int head_dim, hipStream_t stream)
+{
+    return launch_general_norm<kNormSigmoid>(p, head_dim, stream);
+}
+
+}  // namespace attn

@@ -4,14 +4,17 @@
 // peaks are equal), so each lane owns one query row and accumulates with
 // fp32 vector FMAs. A workgroup is one 64-lane wavefront covering 64 query
 // rows of one (sequence, query head); key/value tiles of 32 keys are staged
-// through LDS and read as broadcasts. The score modifications, the band mask
-// with loop splitting, and the base-2 online softmax are the same as in the
-// bf16 kernel (Eq. 1 and 2 of Section 2.2, Appendix A).
+// through LDS and read as broadcasts. The score modifications, the masks with
+// tile skipping, the base-2 online softmax and the ReLU / Sigmoid
+// normalisations are the same as in the bf16 kernel (Eq. 1 and 2 of Section
+// 2.2, Appendix A). On the general mask path each lane derives its row's
+// visible keys (row_vis.h) and the wave visits the union of the rows' tiles.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "kernel_params.h"
 #include "launch.h"
+#include "row_vis.h"
 #include "score_mods.h"
 
 namespace attn {
@@ -23,9 +26,24 @@ constexpr int BM = 64;  // query rows per workgroup (one per lane)
 constexpr int BN = 32;  // keys per tile
 constexpr int NT = 64;
 
-template <int D, bool SOFTCAP, bool ALIBI>
+__device__ __forceinline__ int wave_min(int x)
+{
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) x = min(x, __shfl_xor(x, o));
+    return x;
+}
+
+__device__ __forceinline__ int wave_max(int x)
+{
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) x = max(x, __shfl_xor(x, o));
+    return x;
+}
+
+template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN>
 __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
 {
+    constexpr bool SOFTMAX = NORM == kNormSoftmax;
     __shared__ __attribute__((aligned(16))) float qs[BM][D + 4];  // padded rows
     __shared__ __attribute__((aligned(16))) float ks[BN][D];
     __shared__ __attribute__((aligned(16))) float vs[BN][D];
@@ -77,20 +95,39 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
             *reinterpret_cast<f32x4*>(&qs[tid][4 * c]) = x;
         }
     }
-    int jlo = 1, jhi = 0;
-    if (qi < lq) band_row(p.band, qi, lq, lk, &jlo, &jhi);
+    RowVis rv = {0, 1, 0};
+    int t_lo, t_hi;  // key tiles visited
+    if constexpr (GEN) {
+        if (qi < lq)
+            rv = row_visibility(p.mask_kind, p.band, p.num_global, p.seg, p.num_seg,
+                                p.query_start, qi, lq, lk);
+        const bool any = rv.pfx > 0 || rv.jlo <= rv.jhi;
+        const int first = any ? (rv.pfx > 0 ? 0 : rv.jlo) : 0x3fffffff;
+        const int last = any ? (rv.jlo <= rv.jhi ? rv.jhi : rv.pfx - 1) : -1;
+        t_lo = __builtin_amdgcn_readfirstlane(wave_min(first)) / BN;
+        t_hi = __builtin_amdgcn_readfirstlane(wave_max(last));
+        t_hi = t_hi < 0 ? t_lo : t_hi / BN + 1;
+    } else {
+        if (qi < lq) band_row(p.band, qi, lq, lk, &rv.jlo, &rv.jhi);
+        const TilePlan gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
+        t_lo = gp.lo;
+        t_hi = gp.hi;
+    }
     const int ip = qi + (lk - lq);
-    float slope_log2 = 0.0f;
-    if constexpr (ALIBI) slope_log2 = p.slopes[hq] * kLog2e;
-    constexpr bool MODS = SOFTCAP || ALIBI;
-
-    const TilePlan gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
+    // relative-position reference (see score_u): first visible key for softmax
+    const int jref = SOFTMAX ? (rv.pfx > 0 ? 0 : rv.jlo) : ip;
+    float bias_abs = 0.0f, bias_lin = 0.0f;
+    if constexpr (BIAS == kBiasAlibi || BIAS == kBiasGeneral)
+        if (p.slopes) bias_abs = -p.slopes[hq] * p.unit;
+    if constexpr (BIAS == kBiasRelPos || BIAS == kBiasGeneral)
+        if (p.relpos) bias_lin = p.unit;
+    constexpr bool MODS = SOFTCAP || BIAS != kBiasNone;
     float o[D];
 #pragma unroll
     for (int d = 0; d < D; ++d) o[d] = 0.0f;
     float m_run = -__builtin_inff(), l_run = 0.0f;
 
-    for (int kt = gp.lo; kt < gp.hi; ++kt) {
+    for (int kt = t_lo; kt < t_hi; ++kt) {
         const int j0 = kt * BN;
         __syncthreads();  // previous tile fully consumed
 #pragma unroll
@@ -106,8 +143,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
             *reinterpret_cast<f32x4*>(&vs[r][4 * c]) = vx;
         }
         __syncthreads();
-        if (jlo > jhi || jhi < j0 || jlo > j0 + BN - 1) continue;  // row sees none of the tile
-        const bool full = jlo <= j0 && j0 + BN - 1 <= jhi;
+        const bool band_hit = rv.jlo <= rv.jhi && rv.jhi >= j0 && rv.jlo <= j0 + BN - 1;
+        if (!band_hit && j0 >= rv.pfx) continue;  // row sees none of the tile
+        const bool full = j0 + BN <= rv.pfx || (rv.jlo <= j0 && j0 + BN - 1 <= rv.jhi);
         float s[BN];
 #pragma unroll
         for (int j = 0; j < BN; ++j) s[j] = 0.0f;
@@ -126,12 +164,27 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
         float mx = -__builtin_inff();
 #pragma unroll
         for (int j = 0; j < BN; ++j) {
-            float x = MODS ? score_log2<SOFTCAP, ALIBI>(s[j], p.scale_log2, p.softcap_pre,
-                                                        p.softcap_post, slope_log2, ip, j0 + j)
-                           : s[j] * p.scale_log2;
-            if (!full && (j0 + j < jlo || j0 + j > jhi)) x = -__builtin_inff();
+            float x = MODS ? score_u<SOFTCAP, BIAS>(s[j], p.scale_u, p.softcap_pre, p.softcap_post_u,
+                                                    bias_abs, bias_lin, ip, jref, j0 + j)
+                           : s[j] * p.scale_u;
+            if (!full && !row_sees(rv, j0 + j)) x = -__builtin_inff();
             s[j] = x;
             mx = __builtin_fmaxf(mx, x);
+        }
+        if constexpr (!SOFTMAX) {  // O += act(S) V; the 1/L comes at the end
+#pragma unroll
+            for (int j = 0; j < BN; ++j) {
+                float pe = activation<NORM>(s[j]);
+#pragma unroll
+                for (int c = 0; c < D / 4; ++c) {
+                    f32x4 vx = *reinterpret_cast<const f32x4*>(&vs[j][4 * c]);
+                    o[4 * c + 0] = __builtin_fmaf(pe, vx[0], o[4 * c + 0]);
+                    o[4 * c + 1] = __builtin_fmaf(pe, vx[1], o[4 * c + 1]);
+                    o[4 * c + 2] = __builtin_fmaf(pe, vx[2], o[4 * c + 2]);
+                    o[4 * c + 3] = __builtin_fmaf(pe, vx[3], o[4 * c + 3]);
+                }
+            }
+            continue;
         }
         const float m_new = __builtin_fmaxf(m_run, mx);
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 when m_run = -inf
@@ -155,15 +208,23 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     }
 
     if (qi < lq) {
-        const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+        float inv;
+        if constexpr (SOFTMAX)
+            inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+        else
+            inv = lk > 0 ? 1.0f / (float)lk : 0.0f;
         float* dst = ob + ooff + (int64_t)qi * p.so_s;
 #pragma unroll
         for (int c = 0; c < D / 4; ++c) {
             f32x4 x = {o[4 * c] * inv, o[4 * c + 1] * inv, o[4 * c + 2] * inv, o[4 * c + 3] * inv};
             *reinterpret_cast<f32x4*>(dst + 4 * c) = x;
         }
-        if (p.lse) {
-            float lse = l_run > 0.0f ? (m_run + __builtin_log2f(l_run)) * kLn2 : -__builtin_inff();
+        if (SOFTMAX && p.lse) {
+            float lse = -__builtin_inff();
+            if (l_run > 0.0f) {
+                lse = (m_run + __builtin_log2f(l_run)) * kLn2;
+                if (bias_lin != 0.0f) lse += (float)(ip - jref);
+            }
             int64_t idx = p.cu_q ? (int64_t)hq * p.total_q + qrow0 + qi
                                  : ((int64_t)b * p.hq + hq) * lq + qi;
             p.lse[idx] = lse;
@@ -171,13 +232,34 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     }
 }
 
-template <int D, bool SOFTCAP, bool ALIBI>
+template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN>
 hipError_t launch(const AttnParams& p, hipStream_t stream)
 {
     int64_t blocks = (int64_t)p.num_q_tiles * p.hq * p.batch;
-    hipLaunchKernelGGL((attn_fwd_f32_kernel<D, SOFTCAP, ALIBI>), dim3((unsigned)blocks), dim3(NT),
-                       0, stream, p);
+    hipLaunchKernelGGL((attn_fwd_f32_kernel<D, SOFTCAP, BIAS, NORM, GEN>), dim3((unsigned)blocks),
+                       dim3(NT), 0, stream, p);
     return hipGetLastError();
+}
+
+template <int D, bool SOFTCAP>
+hipError_t launch_d(const AttnParams& p, hipStream_t stream)
+{
+    const bool closed = p.mask_kind >= 0 && p.mask_kind <= 3;  // band masks of plan.h
+    const bool al = p.slopes != nullptr, rp = p.relpos != 0;
+    if (p.norm == kNormSoftmax && closed && !(al && rp)) {
+        if (al) return launch<D, SOFTCAP, kBiasAlibi, kNormSoftmax, false>(p, stream);
+        if (rp) return launch<D, SOFTCAP, kBiasRelPos, kNormSoftmax, false>(p, stream);
+        return launch<D, SOFTCAP, kBiasNone, kNormSoftmax, false>(p, stream);
+    }
+    const bool bias = al || rp;
+    if (p.norm == kNormRelu)
+        return bias ? launch<D, SOFTCAP, kBiasGeneral, kNormRelu, true>(p, stream)
+                    : launch<D, SOFTCAP, kBiasNone, kNormRelu, true>(p, stream);
+    if (p.norm == kNormSigmoid)
+        return bias ? launch<D, SOFTCAP, kBiasGeneral, kNormSigmoid, true>(p, stream)
+                    : launch<D, SOFTCAP, kBiasNone, kNormSigmoid, true>(p, stream);
+    return bias ? launch<D, SOFTCAP, kBiasGeneral, kNormSoftmax, true>(p, stream)
+                : launch<D, SOFTCAP, kBiasNone, kNormSoftmax, true>(p, stream);
 }
 
 }  // namespace
@@ -186,17 +268,9 @@ int f32_block_m() { return BM; }
 
 hipError_t launch_f32(const AttnParams& p, int head_dim, hipStream_t stream)
 {
-    const bool sc = p.softcap > 0.0f, al = p.slopes != nullptr;
-    if (head_dim == 128) {
-        if (sc && al) return launch<128, true, true>(p, stream);
-        if (sc) return launch<128, true, false>(p, stream);
-        if (al) return launch<128, false, true>(p, stream);
-        return launch<128, false, false>(p, stream);
-    }
-    if (sc && al) return launch<64, true, true>(p, stream);
-    if (sc) return launch<64, true, false>(p, stream);
-    if (al) return launch<64, false, true>(p, stream);
-    return launch<64, false, false>(p, stream);
+    const bool sc = p.softcap > 0.0f;
+    if (head_dim == 128) return sc ? launch_d<128, true>(p, stream) : launch_d<128, false>(p, stream);
+    return sc ? launch_d<64, true>(p, stream) : launch_d<64, false>(p, stream);
 }
 
 }  // namespace attn

@@ -1,4 +1,5 @@
-// attn_fwd_bf16.hip -- fused attention forward for bf16 inputs on gfx950.
+// bf16_kernel.h -- fused attention forward for bf16 inputs on gfx950 (kernel
+// template; instantiated by the attn_fwd_bf16*.hip translation units).
 //
 // One workgroup computes BM = 128 query rows of one (sequence, query head):
 // four wavefronts of 32 rows each. It streams the key/value tiles of BN keys
@@ -33,6 +34,18 @@
 //    tile j alongside the score mods, mask and row max of tile j+1. K tiles
 //    are loaded two tiles ahead and V tiles one tile ahead, so each
 //    iteration needs a single barrier.
+//  * Normalisations other than softmax (ReLU, Sigmoid; Appendix A) replace the
+//    exponentials by the activation and drop the running max and sum; O is
+//    scaled by 1/L at the end.
+//  * Masks with a closed-form band (none, causal, sliding window, PrefixLM)
+//    are planned in closed form. The masks built from per-position data
+//    (global sliding window, share question, causal blockwise) take the
+//    general path: every lane derives its row's visible keys (a prefix plus
+//    a band, row_vis.h), the workgroup reduces them to at most two ranges of
+//    key tiles and a fully-visible test per tile, and the loop walks those
+//    ranges, masking only the partial tiles.
+#pragma once
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -40,6 +53,7 @@
 
 #include "kernel_params.h"
 #include "launch.h"
+#include "row_vis.h"
 #include "score_mods.h"
 
 namespace attn {
@@ -57,10 +71,14 @@ constexpr int BM = 128;      // query rows per workgroup
 constexpr int NT = 256;      // threads per workgroup (4 waves)
 constexpr float TAU = 8.0f;  // lazy-rescale threshold, log2 units
 
-template <int D_, int BN_, bool SOFTCAP_, bool ALIBI_>
+// D: head dim; BN: keys per tile; SOFTCAP: soft-cap on; BIAS: kBias*;
+// NORM: kNorm*; GEN: per-row visible ranges (general mask path).
+template <int D_, int BN_, bool SOFTCAP_, int BIAS_, int NORM_, bool GEN_>
 struct Traits {
     static constexpr int D = D_, BN = BN_;
-    static constexpr bool SOFTCAP = SOFTCAP_, ALIBI = ALIBI_, MODS = SOFTCAP_ || ALIBI_;
+    static constexpr bool SOFTCAP = SOFTCAP_, MODS = SOFTCAP_ || BIAS_ != kBiasNone;
+    static constexpr int BIAS = BIAS_, NORM = NORM_;
+    static constexpr bool SOFTMAX = NORM_ == kNormSoftmax, GEN = GEN_;
     static constexpr int NB = BN / 32;                   // 32-key blocks per tile
     static constexpr int ROWB = D * 2;                   // bytes per K/V row in LDS
     static constexpr int TILE = BN * ROWB;               // bytes per K or V tile
@@ -217,12 +235,30 @@ struct WaveState {
     int vaddr[T::DBLK][2];     // LDS byte offsets of this lane's V transpose reads
     f32x16 oacc[T::DBLK];      // O^T accumulator
     f32x16 sa[T::NB], sb[T::NB];  // scores of tiles of even / odd parity
-    float m_run, l_run, alpha;
+    float m_run, l_run, alpha;    // softmax only
     bool need;
-    // row constants
-    int lh, jlo, jhi, ip;
-    float slope_log2;
+    // row constants: visible keys j < pfx (general path) and jlo <= j <= jhi;
+    // key-axis position ip; relative-position reference jref
+    int lh, pfx, jlo, jhi, ip, jref;
+    float bias_abs, bias_lin;  // coefficients of |ip - j| and (jref - j), in units
 };
+
+template <class T>
+__device__ __forceinline__ bool visible(const WaveState<T>& ws, int j)
+{
+    if constexpr (T::GEN)
+        return j < ws.pfx || (j >= ws.jlo && j <= ws.jhi);
+    else
+        return j >= ws.jlo && j <= ws.jhi;
+}
+
+template <class T>
+__device__ __forceinline__ float final_score(float x, const AttnParams& p, const WaveState<T>& ws,
+                                             int j)
+{
+    return score_u<T::SOFTCAP, T::BIAS>(x, p.scale_u, p.softcap_pre, p.softcap_post_u,
+                                         ws.bias_abs, ws.bias_lin, ws.ip, ws.jref, j);
+}
 
 // S^T = K Q^T for the K tile in LDS at `kt`.
 template <class T>
@@ -252,17 +288,16 @@ __device__ __forceinline__ float mods_and_max(f32x16 (&s)[T::NB], const AttnPara
             // element (b, e) is key j0 + 32b + 8lh + e + (e >= 8 ? 8 : 0)
             int j = j0 + 32 * b + 8 * ws.lh + e + (e >= 8 ? 8 : 0);
             float x = s[b][e];
-            if constexpr (T::MODS)
-                x = score_log2<T::SOFTCAP, T::ALIBI>(x, p.scale_log2, p.softcap_pre,
-                                                     p.softcap_post, ws.slope_log2, ws.ip, j);
+            if constexpr (T::MODS) x = final_score<T>(x, p, ws, j);
             if constexpr (MASKED)
-                if (j < ws.jlo || j > ws.jhi) x = -__builtin_inff();
+                if (!visible<T>(ws, j)) x = -__builtin_inff();
             s[b][e] = x;
             mx = __builtin_fmaxf(mx, x);
         }
     }
+    if constexpr (!T::SOFTMAX) return 0.0f;
     mx = pair_max(mx);
-    if constexpr (!T::MODS) mx *= p.scale_log2;  // raw max -> log2 units (scale > 0)
+    if constexpr (!T::MODS) mx *= p.scale_u;  // raw max -> log2 units (scale > 0)
     return mx;
 }
 
@@ -271,6 +306,7 @@ __device__ __forceinline__ float mods_and_max(f32x16 (&s)[T::NB], const AttnPara
 template <class T>
 __device__ __forceinline__ void update_max(WaveState<T>& ws, float mx)
 {
+    if constexpr (!T::SOFTMAX) return;
     const float m_new = __builtin_fmaxf(ws.m_run, mx);
     ws.need = m_new > ws.m_run + TAU;
     ws.alpha = ws.need ? __builtin_amdgcn_exp2f(ws.m_run - m_new) : 1.0f;
@@ -280,6 +316,7 @@ __device__ __forceinline__ void update_max(WaveState<T>& ws, float mx)
 template <class T>
 __device__ __forceinline__ void rescale_if_needed(WaveState<T>& ws)
 {
+    if constexpr (!T::SOFTMAX) return;
     if (__builtin_amdgcn_ballot_w64(ws.need)) {
         ws.l_run *= ws.alpha;
 #pragma unroll
@@ -289,10 +326,22 @@ __device__ __forceinline__ void rescale_if_needed(WaveState<T>& ws)
     }
 }
 
-// P = exp2(S - m) as bf16 B operands of the P V product, plus the row sum.
+// Norm of one score (in units; raw dot product when there are no mods):
+// softmax exp2(S - m), or the ReLU / Sigmoid activation of the natural score.
+template <class T>
+__device__ __forceinline__ float norm_value(float x, float m_use, float scale_u)
+{
+    if constexpr (T::SOFTMAX) {
+        return __builtin_amdgcn_exp2f(T::MODS ? x - m_use : __builtin_fmaf(x, scale_u, -m_use));
+    } else {
+        return activation<T::NORM>(T::MODS ? x : x * scale_u);
+    }
+}
+
+// P = Norm(S) as bf16 B operands of the P V product, plus (softmax) the row sum.
 template <class T>
 __device__ __forceinline__ void exp_tile(f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2], float m_use,
-                                         float scale_log2, float& l_run)
+                                         float scale_u, float& l_run)
 {
     float rs = 0.0f;
 #pragma unroll
@@ -301,17 +350,17 @@ __device__ __forceinline__ void exp_tile(f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][
         for (int u = 0; u < 2; ++u) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                float x0 = s[b][8 * u + 2 * q], x1 = s[b][8 * u + 2 * q + 1];
-                float y0 = T::MODS ? x0 - m_use : __builtin_fmaf(x0, scale_log2, -m_use);
-                float y1 = T::MODS ? x1 - m_use : __builtin_fmaf(x1, scale_log2, -m_use);
-                float p0 = __builtin_amdgcn_exp2f(y0), p1 = __builtin_amdgcn_exp2f(y1);
-                rs += p0;
-                rs += p1;
+                float p0 = norm_value<T>(s[b][8 * u + 2 * q], m_use, scale_u);
+                float p1 = norm_value<T>(s[b][8 * u + 2 * q + 1], m_use, scale_u);
+                if constexpr (T::SOFTMAX) {
+                    rs += p0;
+                    rs += p1;
+                }
                 pw[b][u][q] = pack_bf16(p0, p1);
             }
         }
     }
-    l_run += rs;
+    if constexpr (T::SOFTMAX) l_run += rs;
 }
 
 // O^T += V^T P^T for the V tile in LDS at `vt`.
@@ -389,17 +438,17 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             read_v(i + PF - QK);
         static_for<EQ / 2>([&](auto kc) __attribute__((always_inline)) {
             constexpr int el = i * EQ + 2 * kc.value, bb = el / 16, e = el % 16;
-            const float x0 = sc[bb][e], x1 = sc[bb][e + 1];
-            const float y0 = T::MODS ? x0 - m_use : __builtin_fmaf(x0, p.scale_log2, -m_use);
-            const float y1 = T::MODS ? x1 - m_use : __builtin_fmaf(x1, p.scale_log2, -m_use);
-            const float p0 = __builtin_amdgcn_exp2f(y0), p1 = __builtin_amdgcn_exp2f(y1);
-            rs += p0;
-            rs += p1;
+            const float p0 = norm_value<T>(sc[bb][e], m_use, p.scale_u);
+            const float p1 = norm_value<T>(sc[bb][e + 1], m_use, p.scale_u);
+            if constexpr (T::SOFTMAX) {
+                rs += p0;
+                rs += p1;
+            }
             pw[bb][e / 8][(e % 8) / 2] = pack_bf16(p0, p1);
         });
         __builtin_amdgcn_sched_barrier(0);
     });
-    ws.l_run += rs;
+    if constexpr (T::SOFTMAX) ws.l_run += rs;
     static_for<PV>([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = ic.value;
         constexpr int b = i / (2 * DBLK), u = (i / DBLK) % 2, d = i % DBLK;
@@ -414,19 +463,19 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             // element (bb, e) is key jn + 32bb + 8lh + e + (e >= 8 ? 8 : 0)
             const int j = jn + 32 * bb + 8 * ws.lh + e + (e >= 8 ? 8 : 0);
             float x = sn[bb][e];
-            if constexpr (T::MODS)
-                x = score_log2<T::SOFTCAP, T::ALIBI>(x, p.scale_log2, p.softcap_pre, p.softcap_post,
-                                                     ws.slope_log2, ws.ip, j);
+            if constexpr (T::MODS) x = final_score<T>(x, p, ws, j);
             if constexpr (MASKED)
-                if (j < ws.jlo || j > ws.jhi) x = -__builtin_inff();
+                if (!visible<T>(ws, j)) x = -__builtin_inff();
             sn[bb][e] = x;
-            mx = __builtin_fmaxf(mx, x);
+            if constexpr (T::SOFTMAX) mx = __builtin_fmaxf(mx, x);
         });
         __builtin_amdgcn_sched_barrier(0);
     });
-    mx = pair_max(mx);
-    if constexpr (!T::MODS) mx *= p.scale_log2;  // raw max -> log2 units (scale > 0)
-    update_max(ws, mx);
+    if constexpr (T::SOFTMAX) {
+        mx = pair_max(mx);
+        if constexpr (!T::MODS) mx *= p.scale_u;  // raw max -> log2 units (scale > 0)
+        update_max(ws, mx);
+    }
 }
 
 // The last step of the key loop: exponentials and P V of the current tile.
@@ -435,8 +484,84 @@ __device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, f
                                           const AttnParams& p, float m_use)
 {
     u32x4 pw[T::NB][2];
-    exp_tile<T>(sc, pw, m_use, p.scale_log2, ws.l_run);
+    exp_tile<T>(sc, pw, m_use, p.scale_u, ws.l_run);
     pv_tile<T>(vread, pw, ws);
+}
+
+__device__ __forceinline__ int wave_min(int x)
+{
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) x = min(x, __shfl_xor(x, o));
+    return x;
+}
+
+__device__ __forceinline__ int wave_max(int x)
+{
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) x = max(x, __shfl_xor(x, o));
+    return x;
+}
+
+// Key tiles visited by a workgroup on the general path: the virtual index
+// n < len1 maps to tile r1_lo + n, and n >= len1 to tile r2_lo + n - len1.
+// A tile t is fully visible for every row when (t + 1) * BN <= pmin or
+// lomax <= t * BN and t * BN + BN - 1 <= himin.
+struct TileRanges {
+    int r1_lo, len1, r2_lo, n;
+    int pmin, lomax, himin;
+};
+
+// Reduce the rows' visible ranges over the workgroup (wave reductions, then
+// one LDS exchange) into the tile ranges. Rows past the end (valid = false)
+// do not take part.
+template <int BN>
+__device__ TileRanges plan_general(RowVis r, bool valid, int (*red)[8], int wave, int lane)
+{
+    const int big = 0x3fffffff;
+    const bool band = valid && r.jlo <= r.jhi;
+    int v[6];
+    v[0] = valid ? r.pfx : 0;                 // max prefix
+    v[1] = valid ? -r.pfx : -big;             // -(min prefix)
+    v[2] = band ? -r.jlo : -big;              // -(min band start)
+    v[3] = valid ? (band ? r.jlo : big) : -big;  // max band start (empty band: none full)
+    v[4] = band ? r.jhi : -big;               // max band end
+    v[5] = valid ? (band ? -r.jhi : big) : -big; // -(min band end)
+#pragma unroll
+    for (int i = 0; i < 6; ++i) v[i] = wave_max(v[i]);
+    if (lane == 0) {
+#pragma unroll
+        for (int i = 0; i < 6; ++i) red[wave][i] = v[i];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 6; ++i)
+        v[i] = __builtin_amdgcn_readfirstlane(
+            max(max(red[0][i], red[1][i]), max(red[2][i], red[3][i])));
+    TileRanges t;
+    const int pmax = v[0], lomin = -v[2], himax = v[4];
+    t.pmin = -v[1];
+    t.lomax = v[3];
+    t.himin = -v[5];
+    const int a_hi = (pmax + BN - 1) / BN;  // prefix tiles [0, a_hi)
+    int b_lo = 0, b_hi = 0;                 // band tiles [b_lo, b_hi)
+    if (lomin <= himax) {
+        b_lo = lomin / BN;
+        b_hi = himax / BN + 1;
+    }
+    t.r2_lo = 0;
+    if (b_lo >= b_hi) {
+        t.r1_lo = 0;
+        t.len1 = a_hi;
+    } else if (a_hi >= b_lo) {  // overlapping or adjacent: one range
+        t.r1_lo = a_hi > 0 ? 0 : b_lo;
+        t.len1 = max(a_hi, b_hi) - t.r1_lo;
+    } else {
+        t.r1_lo = 0;
+        t.len1 = a_hi;
+        t.r2_lo = b_lo;
+    }
+    t.n = t.len1 + (b_lo < b_hi && a_hi < b_lo ? b_hi - b_lo : 0);
+    return t;
 }
 
 template <class T>
@@ -530,13 +655,50 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vbase, slice_bytes(p.sv_s));
     const uint32_t krow = (uint32_t)(p.sk_s * 2), vrow = (uint32_t)(p.sv_s * 2);
 
-    // Visible key interval of this lane's row; rows past the end see nothing.
+    // Visible keys of this lane's row; rows past the end see nothing.
+    ws.ip = qi + (lk - lq);
+    ws.pfx = 0;
     ws.jlo = 1;
     ws.jhi = 0;
-    if (qi < lq) band_row(p.band, qi, lq, lk, &ws.jlo, &ws.jhi);
-    ws.ip = qi + (lk - lq);
-    ws.slope_log2 = 0.0f;
-    if constexpr (T::ALIBI) ws.slope_log2 = p.slopes[it.hq] * kLog2e;
+    TileRanges tr = {};
+    int jbeg, jend;
+    TilePlan gp = {};
+    if constexpr (T::GEN) {
+        __shared__ int red[4][8];
+        const int32_t* seg = p.seg;
+        if (p.seg) {  // stage the segment starts in the (not yet used) V buffer 1
+            int32_t* sl = reinterpret_cast<int32_t*>(lds_v1);
+            for (int i = tid; i < p.num_seg; i += NT) sl[i] = p.seg[i];
+            __syncthreads();
+            seg = sl;
+        }
+        RowVis rv = {0, 1, 0};
+        if (qi < lq)
+            rv = row_visibility(p.mask_kind, p.band, p.num_global, seg, p.num_seg, p.query_start,
+                                qi, lq, lk);
+        ws.pfx = rv.pfx;
+        ws.jlo = rv.jlo;
+        ws.jhi = rv.jhi;
+        tr = plan_general<BN>(rv, qi < lq, red, wave, lane);
+        jbeg = 0;
+        jend = tr.n;
+    } else {
+        if (qi < lq) band_row(p.band, qi, lq, lk, &ws.jlo, &ws.jhi);
+        gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
+        jbeg = gp.lo;
+        jend = gp.hi;
+    }
+    // Relative-position reference: the row's first visible key for softmax
+    // (largest bias; the shift is added back to the LSE), i' otherwise.
+    ws.jref = T::SOFTMAX ? (ws.pfx > 0 ? 0 : ws.jlo) : ws.ip;
+    ws.bias_abs = 0.0f;
+    ws.bias_lin = 0.0f;
+    if constexpr (T::BIAS == kBiasAlibi) ws.bias_abs = -p.slopes[it.hq] * p.unit;
+    if constexpr (T::BIAS == kBiasRelPos) ws.bias_lin = p.unit;
+    if constexpr (T::BIAS == kBiasGeneral) {
+        if (p.slopes) ws.bias_abs = -p.slopes[it.hq] * p.unit;
+        if (p.relpos) ws.bias_lin = p.unit;
+    }
 
 #pragma unroll
     for (int d = 0; d < T::DBLK; ++d) ws.oacc[d] = f32x16{};
@@ -545,27 +707,40 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     ws.alpha = 1.0f;
     ws.need = false;
 
-    const TilePlan gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
-    const int lo = gp.lo, hi = gp.hi;
+    // Key tile of loop index n, and (general path) whether it is fully visible.
+    auto tile_of = [&](int n) __attribute__((always_inline)) -> int {
+        if constexpr (T::GEN)
+            return n < tr.len1 ? tr.r1_lo + n : tr.r2_lo + (n - tr.len1);
+        else
+            return n;
+    };
+    auto gen_full = [&](int t) __attribute__((always_inline)) -> bool {
+        return (t + 1) * BN <= tr.pmin || (tr.lomax <= t * BN && t * BN + BN - 1 <= tr.himin);
+    };
 
-    if (hi > lo) {
+    if (jend > jbeg) {
         // Prologue: K_lo, V_lo -> buffers 0, K_lo+1 -> K buffer 1; S_lo.
-        issue_tile<T>(lds_k0, krs, lo * BN, krow, klp, wave);
-        issue_tile<T>(lds_v0, vrs, lo * BN, vrow, vlp, wave);
-        if (lo + 1 < hi) issue_tile<T>(lds_k1, krs, (lo + 1) * BN, krow, klp, wave);
+        const int t0 = tile_of(jbeg);
+        issue_tile<T>(lds_k0, krs, t0 * BN, krow, klp, wave);
+        issue_tile<T>(lds_v0, vrs, t0 * BN, vrow, vlp, wave);
+        if (jbeg + 1 < jend) issue_tile<T>(lds_k1, krs, tile_of(jbeg + 1) * BN, krow, klp, wave);
         __builtin_amdgcn_s_waitcnt(0);  // this thread's loads have landed in LDS
         __syncthreads();
         qk_tile<T>(lds_k0, ws, ws.sa);
-        const bool masked_lo = !(lo >= gp.full_lo && lo < gp.full_hi);
-        float mx = masked_lo ? mods_and_max<T, true>(ws.sa, p, ws, lo * BN)
-                             : mods_and_max<T, false>(ws.sa, p, ws, lo * BN);
+        bool masked_lo;
+        if constexpr (T::GEN)
+            masked_lo = !gen_full(t0);
+        else
+            masked_lo = !(t0 >= gp.full_lo && t0 < gp.full_hi);
+        float mx = masked_lo ? mods_and_max<T, true>(ws.sa, p, ws, t0 * BN)
+                             : mods_and_max<T, false>(ws.sa, p, ws, t0 * BN);
         update_max(ws, mx);
         __syncthreads();  // K buffer 0 is reloaded in the first iteration
 
-        // Iteration j with parity PAR = (j - lo) & 1 reads K_{j+1} from K
+        // Iteration j with parity PAR = (j - jbeg) & 1 reads K_{j+1} from K
         // buffer PAR^1 and V_j from V buffer PAR, and loads K_{j+2} into K
-        // buffer PAR and V_{j+1} into V buffer PAR^1. MASKED is the class of
-        // tile j+1.
+        // buffer PAR and V_{j+1} into V buffer PAR^1 (j counts visited
+        // tiles). MASKED is the class of tile j+1.
         auto iteration = [&](auto par_c, auto masked_c, int j) __attribute__((always_inline)) {
             constexpr int PAR = decltype(par_c)::value;
             constexpr bool MASKED = decltype(masked_c)::value;
@@ -574,19 +749,20 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             char* vread = PAR ? lds_v1 : lds_v0;
             char* vwrite = PAR ? lds_v0 : lds_v1;
             rescale_if_needed(ws);
-            if (j + 2 < hi) issue_tile<T>(kwrite, krs, (j + 2) * BN, krow, klp, wave);
-            issue_tile<T>(vwrite, vrs, (j + 1) * BN, vrow, vlp, wave);
+            const int t1 = tile_of(j + 1);
+            if (j + 2 < jend) issue_tile<T>(kwrite, krs, tile_of(j + 2) * BN, krow, klp, wave);
+            issue_tile<T>(vwrite, vrs, t1 * BN, vrow, vlp, wave);
             const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
             if constexpr (PAR == 0)
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, (j + 1) * BN);
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, t1 * BN);
             else
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, (j + 1) * BN);
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, t1 * BN);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
         };
-        // Loop splitting (Section 3.4): leading partial tiles, check-free full
-        // tiles, trailing partial tiles; each phase has a branch-free body.
-        int j = lo, par = 0;
+        // Loop splitting (Section 3.4): runs of partial and check-free tiles,
+        // each phase with a branch-free body.
+        int j = jbeg, par = 0;
         auto phase = [&](auto masked_c, int end) __attribute__((always_inline)) {  // iterations while tile j+1 < end
             if (par && j + 1 < end) {
                 iteration(Parity<1>{}, masked_c, j);
@@ -604,9 +780,28 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
                 par = 1;
             }
         };
-        phase(Bool<true>{}, gp.full_lo);
-        phase(Bool<false>{}, gp.full_hi);
-        phase(Bool<true>{}, hi);
+        if constexpr (T::GEN) {
+            // Visited tiles fall into at most four runs: check-free prefix
+            // tiles, partial tiles, check-free band tiles, partial tiles. Any
+            // further check-free tile goes through the masked body, which is
+            // correct for every tile.
+            auto run_end = [&](int from, bool full) __attribute__((always_inline)) {
+                int e = from;
+                while (e < jend && gen_full(tile_of(e)) == full) ++e;
+                return e;
+            };
+            const int e1 = run_end(jbeg + 1, true);
+            const int e2 = run_end(e1, false);
+            const int e3 = run_end(e2, true);
+            phase(Bool<false>{}, e1);
+            phase(Bool<true>{}, e2);
+            phase(Bool<false>{}, e3);
+            phase(Bool<true>{}, jend);
+        } else {
+            phase(Bool<true>{}, gp.full_lo);
+            phase(Bool<false>{}, gp.full_hi);
+            phase(Bool<true>{}, jend);
+        }
         rescale_if_needed(ws);
         const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
         if (par)
@@ -615,10 +810,18 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             last_step<T>(lds_v0, ws, ws.sa, p, m_use);
     }
 
-    // Epilogue: O = O^T / l, LSE = (m + log2 l) ln 2. Lane halves hold halves of the row sum.
-    const float l_tot = pair_sum(ws.l_run);
+    // Epilogue. Softmax: O = O^T / l, LSE = (m + log2 l) ln 2 (+ the relative
+    // position shift); lane halves hold halves of the row sum. ReLU / Sigmoid:
+    // O = O^T / L.
+    float inv = 0.0f;
+    float l_tot = 0.0f;
+    if constexpr (T::SOFTMAX) {
+        l_tot = pair_sum(ws.l_run);
+        inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+    } else {
+        inv = lk > 0 ? 1.0f / (float)lk : 0.0f;
+    }
     if (qi < lq) {
-        const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
         __bf16* orow = ob + ooff + (int64_t)qi * p.so_s;
 #pragma unroll
         for (int d = 0; d < T::DBLK; ++d) {
@@ -631,11 +834,17 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
                 *reinterpret_cast<u32x4*>(orow + 32 * d + 16 * u + 8 * lh) = w;
             }
         }
-        if (p.lse && lh == 0) {
-            float lse = l_tot > 0.0f ? (ws.m_run + __builtin_log2f(l_tot)) * kLn2 : -__builtin_inff();
-            int64_t idx = p.cu_q ? (int64_t)it.hq * p.total_q + qrow0 + qi
-                                 : ((int64_t)it.b * p.hq + it.hq) * lq + qi;
-            p.lse[idx] = lse;
+        if constexpr (T::SOFTMAX) {
+            if (p.lse && lh == 0) {
+                float lse = -__builtin_inff();
+                if (l_tot > 0.0f) {
+                    lse = (ws.m_run + __builtin_log2f(l_tot)) * kLn2;
+                    if (ws.bias_lin != 0.0f) lse += (float)(ws.ip - ws.jref);
+                }
+                int64_t idx = p.cu_q ? (int64_t)it.hq * p.total_q + qrow0 + qi
+                                     : ((int64_t)it.b * p.hq + it.hq) * lq + qi;
+                p.lse[idx] = lse;
+            }
         }
     }
 }
@@ -652,32 +861,32 @@ constexpr int key_tile_width(int)
 #endif
 }
 
-template <int D, bool SOFTCAP, bool ALIBI>
-hipError_t launch(const AttnParams& p, hipStream_t stream)
+template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN>
+hipError_t launch_variant(const AttnParams& p, hipStream_t stream)
 {
-    using T = Traits<D, key_tile_width(D), SOFTCAP, ALIBI>;
+    using T = Traits<D, key_tile_width(D), SOFTCAP, BIAS, NORM, GEN>;
     int64_t blocks = (int64_t)p.num_q_tiles * p.hq * p.batch;
     hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)blocks), dim3(NT), 0, stream, p);
     return hipGetLastError();
 }
 
-}  // namespace
-
-int bf16_block_m() { return BM; }
-
-hipError_t launch_bf16(const AttnParams& p, int head_dim, hipStream_t stream)
+// The general-path instantiations of one normalisation: head dim, soft-cap,
+// and a runtime-coefficient bias when ALiBi or the relative position is on.
+template <int NORM>
+hipError_t launch_general_norm(const AttnParams& p, int head_dim, hipStream_t stream)
 {
-    const bool sc = p.softcap > 0.0f, al = p.slopes != nullptr;
+    const bool sc = p.softcap > 0.0f, bias = p.slopes != nullptr || p.relpos != 0;
     if (head_dim == 128) {
-        if (sc && al) return launch<128, true, true>(p, stream);
-        if (sc) return launch<128, true, false>(p, stream);
-        if (al) return launch<128, false, true>(p, stream);
-        return launch<128, false, false>(p, stream);
+        if (sc && bias) return launch_variant<128, true, kBiasGeneral, NORM, true>(p, stream);
+        if (sc) return launch_variant<128, true, kBiasNone, NORM, true>(p, stream);
+        if (bias) return launch_variant<128, false, kBiasGeneral, NORM, true>(p, stream);
+        return launch_variant<128, false, kBiasNone, NORM, true>(p, stream);
     }
-    if (sc && al) return launch<64, true, true>(p, stream);
-    if (sc) return launch<64, true, false>(p, stream);
-    if (al) return launch<64, false, true>(p, stream);
-    return launch<64, false, false>(p, stream);
+    if (sc && bias) return launch_variant<64, true, kBiasGeneral, NORM, true>(p, stream);
+    if (sc) return launch_variant<64, true, kBiasNone, NORM, true>(p, stream);
+    if (bias) return launch_variant<64, false, kBiasGeneral, NORM, true>(p, stream);
+    return launch_variant<64, false, kBiasNone, NORM, true>(p, stream);
 }
 
+}  // namespace
 }  // namespace attn

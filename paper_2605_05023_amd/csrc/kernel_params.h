@@ -26,10 +26,21 @@ struct AttnParams {
     int64_t sk_b, sk_h, sk_s;
     int64_t sv_b, sv_h, sv_s;
     int64_t so_b, so_h, so_s;
-    KeyBand band;            // mask as a key band
+    KeyBand band;            // closed-form masks as a key band
+    // Masks whose visible keys come from per-row data (general path).
+    int32_t mask_kind;       // attn_mask_kind_t
+    int32_t num_global;      // global sliding window: positions 0..num_global-1
+    const int32_t* seg;      // segment start positions (device), or null
+    int32_t num_seg;
+    int32_t query_start;     // causal blockwise: first test-query position
+    int32_t norm;            // attn_norm_kind_t
+    int32_t relpos;          // add (i' - j) to the score
+    // Scores are kept in "units": base-2 logits for softmax (unit = log2 e),
+    // natural values for ReLU / Sigmoid (unit = 1).
+    float unit;
     float scale;             // multiplies q . k
-    float scale_log2;        // scale * log2(e)
+    float scale_u;           // scale * unit
     float softcap;           // C, 0 = off
     float softcap_pre;       // scale / C
-    float softcap_post;      // C * log2(e)
+    float softcap_post_u;    // C * unit
 };

@@ -1,13 +1,16 @@
 // plan.h -- key-tile planning for one block of query rows (host and device).
 //
-// The mask of every supported variant is a band on the key axis: query row i
+// The masks with a closed-form plan are bands on the key axis: query row i
 // of a sequence with lq queries and lk keys sits at key position
 // i' = i + (lk - lq) and sees keys j with lo(i) <= j <= hi(i), where
 //   lo(i) = max(0, i' - window_left)   (0 when window_left < 0)
-//   hi(i) = min(lk - 1, i' + window_right)  (lk - 1 when window_right < 0).
-// No-mask is the band (-1, -1) and causal is (-1, 0). Both bounds grow with
-// i, so the keys seen by a run of consecutive rows form one interval and a
-// key tile is either untouched, fully visible for every row, or partial.
+//   hi(i) = min(lk - 1, max(i' + window_right, prefix - 1))
+//           (lk - 1 when window_right < 0; prefix only with lo = 0).
+// No-mask is the band (-1, -1), causal is (-1, 0) and PrefixLM (Appendix A,
+// "PrefixLM") is causal plus a prefix: keys j < L_p are visible to every row,
+// so hi(i) = max(i', L_p - 1). Both bounds grow with i, so the keys seen by a
+// run of consecutive rows form one interval and a key tile is either
+// untouched, fully visible for every row, or partial.
 // Splitting the key loop at those boundaries keeps the element mask out of
 // the fully visible tiles and skips untouched ones (loop splitting of the
 // iteration space, Section 3.4, Fig. 4; block-level skipping, Appendix C).
@@ -24,6 +27,7 @@
 struct KeyBand {
     int32_t wl;  // max i' - j, < 0 = unbounded
     int32_t wr;  // max j - i', < 0 = unbounded
+    int32_t pl;  // keys j < pl are visible to every row (PrefixLM); needs wl < 0
 };
 
 // Visible key interval [lo, hi] of row i (empty when lo > hi).
@@ -32,6 +36,7 @@ ATTN_HD void band_row(KeyBand b, int32_t i, int32_t lq, int32_t lk, int32_t* lo,
     int32_t ip = i + (lk - lq);
     int32_t l = b.wl < 0 ? 0 : ip - b.wl;
     int32_t h = b.wr < 0 ? lk - 1 : ip + b.wr;
+    if (h < b.pl - 1) h = b.pl - 1;
     *lo = l < 0 ? 0 : l;
     *hi = h > lk - 1 ? lk - 1 : h;
 }

@@ -1,9 +1,12 @@
-// score_mods.h -- device helpers for the Score stage of attention.
+// score_mods.h -- device helpers for the Score and Norm stages of attention.
 //
 // Score modifications act on the scaled raw score s = scale * q . k before
 // the mask (Appendix A, "Score Modifications"): the soft-cap C * tanh(s / C)
-// ("Softcap Attention"), then the ALiBi bias -slope_h * |i' - j|. The kernels
-// run the softmax in base 2, so a score leaves here multiplied by log2(e).
+// ("Softcap Attention"), then the additive position biases: ALiBi
+// -slope_h * |i' - j| and the relative position term (i' - j) ("Relative
+// Position Embeddings"). The softmax kernels run in base 2, so their scores
+// carry a factor log2(e) ("unit"); ReLU and Sigmoid normalisation (Appendix
+// A, "Normalization Variants") work on natural scores (unit 1).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -12,6 +15,17 @@ namespace attn {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+
+// Additive position bias selected at compile time.
+enum : int {
+    kBiasNone = 0,
+    kBiasAlibi = 1,    // bias_abs * |i' - j|, bias_abs = -slope_h * unit
+    kBiasRelPos = 2,   // bias_lin * (jref - j), bias_lin = unit
+    kBiasGeneral = 3,  // both terms, coefficients possibly zero
+};
+
+// Normalisation selected at compile time.
+enum : int { kNormSoftmax = 0, kNormRelu = 1, kNormSigmoid = 2 };
 
 // tanh for fp32 with small absolute and relative error over the whole line.
 // |x| < 0.4: Taylor series of tanh about 0 (coefficients from the Bernoulli
@@ -35,23 +49,39 @@ __device__ __forceinline__ float tanh_f32(float x)
     return __builtin_copysignf(r, x);
 }
 
-// Final score in log2 units for a raw dot product `dot` of query position ip
-// (on the key axis) and key j.
-template <bool SOFTCAP, bool ALIBI>
-__device__ __forceinline__ float score_log2(float dot, float scale_log2, float softcap_pre,
-                                            float softcap_post, float slope_log2, int ip, int j)
+// Final score, in units, of a raw dot product `dot` for the query at key-axis
+// position ip and key j. The relative-position term is taken against jref:
+// softmax is unchanged by a per-row constant, so the softmax kernels use
+// jref = the row's first visible key (the largest bias, keeping the dominant
+// scores small in magnitude) and add (ip - jref) back to the LSE; the other
+// normalisations use jref = ip, the literal (i' - j).
+template <bool SOFTCAP, int BIAS>
+__device__ __forceinline__ float score_u(float dot, float scale_u, float softcap_pre,
+                                         float softcap_post_u, float bias_abs, float bias_lin,
+                                         int ip, int jref, int j)
 {
     float t;
-    if constexpr (SOFTCAP) {
-        t = softcap_post * tanh_f32(dot * softcap_pre);
-    } else {
-        t = dot * scale_log2;
-    }
-    if constexpr (ALIBI) {
-        int rel = ip - j;
-        t = __builtin_fmaf(-slope_log2, (float)(rel < 0 ? -rel : rel), t);
-    }
+    if constexpr (SOFTCAP)
+        t = softcap_post_u * tanh_f32(dot * softcap_pre);
+    else
+        t = dot * scale_u;
+    if constexpr (BIAS == kBiasAlibi || BIAS == kBiasGeneral)
+        t = __builtin_fmaf(bias_abs, __builtin_fabsf((float)(ip - j)), t);
+    if constexpr (BIAS == kBiasRelPos || BIAS == kBiasGeneral)
+        t = __builtin_fmaf(bias_lin, (float)(jref - j), t);
     return t;
+}
+
+// ReLU(x) and Sigmoid(x) of a natural score; a masked score (-inf) maps to 0.
+template <int NORM>
+__device__ __forceinline__ float activation(float x)
+{
+    if constexpr (NORM == kNormRelu) {
+        return __builtin_fmaxf(x, 0.0f);
+    } else {
+        // 1 / (1 + e^-x); e^-x = +inf for x = -inf gives 0
+        return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -kLog2e));
+    }
 }
 
 }  // namespace attn

@@ -111,6 +111,27 @@ CASES = [
     ("slice beyond 2 GiB", lambda d: (setattr(d, "seqlen_k", 1 << 20), setattr(d, "stride_k_s", 1 << 12)),
      "ATTN_ERR_UNSUPPORTED"),
     ("cu_k without cu_q", lambda d: setattr(d, "cu_seqlens_k", P), "ATTN_ERR_BAD_SHAPE"),
+    ("mask kind 7", lambda d: setattr(d, "mask_kind", 7), "ATTN_ERR_BAD_VARIANT"),
+    ("mask kind < 0", lambda d: setattr(d, "mask_kind", -1), "ATTN_ERR_BAD_VARIANT"),
+    ("norm kind 3", lambda d: setattr(d, "norm_kind", 3), "ATTN_ERR_BAD_VARIANT"),
+    ("norm kind < 0", lambda d: setattr(d, "norm_kind", -1), "ATTN_ERR_BAD_VARIANT"),
+    ("relative_position 2", lambda d: setattr(d, "relative_position", 2), "ATTN_ERR_BAD_VARIANT"),
+    ("prefix < 0", lambda d: (setattr(d, "mask_kind", 3), setattr(d, "prefix_len", -1)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("global window < -1", lambda d: (setattr(d, "mask_kind", 4), setattr(d, "window_left", -3)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("num_global < 0", lambda d: (setattr(d, "mask_kind", 4), setattr(d, "num_global", -1)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("no segments", lambda d: (setattr(d, "mask_kind", 5), setattr(d, "segment_starts", P),
+                               setattr(d, "num_segments", 0)), "ATTN_ERR_BAD_VARIANT"),
+    ("too many segments", lambda d: (setattr(d, "mask_kind", 6), setattr(d, "segment_starts", P),
+                                     setattr(d, "num_segments", _abi.ATTN_MAX_SEGMENTS + 1)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("query_start < 0", lambda d: (setattr(d, "mask_kind", 6), setattr(d, "segment_starts", P),
+                                   setattr(d, "num_segments", 2), setattr(d, "query_start", -4)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("segments missing", lambda d: (setattr(d, "mask_kind", 5), setattr(d, "num_segments", 3)),
+     "ATTN_ERR_NULL_PTR"),
 ]
 
 

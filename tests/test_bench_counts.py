@@ -1,0 +1,46 @@
+"""bench.py's closed-form count of visible (query, key) pairs -- the FLOP
+numerator of every reported TFLOP/s -- against the CPU oracle's mask (with
+zero queries P > 0 exactly on visible pairs), for every mask kind."""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+import bench  # noqa: E402
+from paper_2605_05023_amd.workloads import WORKLOADS, make_inputs  # noqa: E402
+
+NAMES = ["causal_bf16", "gqa_swa_bf16", "alibi_softcap_bf16", "prefixlm_bf16",
+         "global_window_bf16", "share_question_bf16", "causal_blockwise_bf16", "relu_bf16"]
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_row_counts_match_oracle_mask(name):
+    wl = WORKLOADS[name]
+    for S in (1, 37, 300):
+        small = dataclasses.replace(
+            wl, seqlen=S, batch=1, hq=1, hkv=1, prefix_len=min(wl.prefix_len, S // 3),
+            query_start=min(wl.query_start, 2 * S // 3), num_global=min(wl.num_global, 5),
+            window_left=min(wl.window_left, 20) if wl.window_left >= 0 else -1,
+            window_right=min(wl.window_right, 20) if wl.window_right >= 0 else -1)
+        inp = make_inputs(small)
+        kw = inp.oracle_mask_kwargs()
+        kw["norm"] = oracle.NORM_SOFTMAX
+        q = torch.zeros((1, 1, S, 4))
+        kv = torch.ones((1, 1, S, 4))
+        _, _, p = oracle.attention(q, kv, kv, scale=1.0, mask=small.mask,
+                                   window_left=small.window_left,
+                                   window_right=small.window_right, want_probs=True, **kw)
+        assert np.array_equal((p[0, 0] > 0).sum(1), bench.row_counts(inp, S)), (name, S)
+
+
+def test_headline_pair_counts():
+    # causal S(S+1)/2 x 64 heads; window: sum_i min(i+1, 1024) x 64 heads
+    assert bench.visible_pairs(make_inputs(WORKLOADS["causal_bf16"])) == 2048 * 2049 // 2 * 64
+    assert bench.visible_pairs(make_inputs(WORKLOADS["gqa_swa_bf16"])) == \
+        sum(min(i + 1, 1024) for i in range(8192)) * 64
