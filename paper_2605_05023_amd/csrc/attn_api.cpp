@@ -252,6 +252,9 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.softcap = d.softcap;
     p.softcap_pre = d.softcap > 0.0f ? d.scale / d.softcap : 0.0f;
     p.softcap_post_u = d.softcap * p.unit;
+    // Longest tiles first: the last query tiles under causal-like masks, the
+    // first ones when global rows (which see every key) sit at the start.
+    p.q_order = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.num_global > 0 ? 1 : 0;
     // Keep each kv-head group on one XCD when the groups divide evenly.
     p.map_mode = ((int64_t)d.batch * d.num_kv_heads) % 8 == 0 ? 1 : 0;
     if (const char* env = std::getenv("ATTN_MAP_MODE")) {

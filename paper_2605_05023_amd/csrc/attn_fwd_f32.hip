@@ -51,7 +51,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     const int tid = threadIdx.x;
     const int nbh = p.batch * p.hq;
     const int w = blockIdx.x;
-    const int qt = p.num_q_tiles - 1 - w / nbh;
+    const int qt = p.q_order ? w / nbh : p.num_q_tiles - 1 - w / nbh;
     const int b = (w % nbh) / p.hq, hq = (w % nbh) % p.hq;
 
     int lq, lk;

@@ -200,8 +200,9 @@ struct Bool {
 };
 
 // Map the hardware workgroup id to (sequence, query head, query tile).
-// Query tiles are issued longest-first (the last tiles of a causal sequence
-// see the most keys). Mode 1 keeps all query heads of a kv-head group on one
+// Query tiles are issued longest-first: the last tiles of a causal sequence
+// see the most keys, so the order is descending unless the host asks for
+// ascending (q_order = 1: the first tiles are the heaviest, e.g. global rows). Mode 1 keeps all query heads of a kv-head group on one
 // XCD (workgroup ids are dealt round-robin over the 8 XCDs), so their K/V
 // tiles are shared through that XCD's L2.
 __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
@@ -217,12 +218,12 @@ __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
         int g = x + 8 * gi;
         it.b = g / p.hkv;
         it.hq = (g % p.hkv) * p.group + r;
-        it.qt = p.num_q_tiles - 1 - qt_rev;
+        it.qt = p.q_order ? qt_rev : p.num_q_tiles - 1 - qt_rev;
     } else {
         int qt_rev = w / nbh, rem = w % nbh;
         it.b = rem / p.hq;
         it.hq = rem % p.hq;
-        it.qt = p.num_q_tiles - 1 - qt_rev;
+        it.qt = p.q_order ? qt_rev : p.num_q_tiles - 1 - qt_rev;
     }
     return it;
 }
