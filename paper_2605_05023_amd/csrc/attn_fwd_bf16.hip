@@ -11,26 +11,28 @@ int bf16_block_m() { return BM; }
 
 namespace {
 
-template <int D>
+template <int D, bool LEFT>
 hipError_t launch_closed_form(const AttnParams& p, hipStream_t stream)
 {
     const bool sc = p.softcap > 0.0f;
     const int bias = p.slopes ? kBiasAlibi : (p.relpos ? kBiasRelPos : kBiasNone);
     if (sc) {
-        if (bias == kBiasAlibi) return launch_variant<D, true, kBiasAlibi, kNormSoftmax, false>(p, stream);
-        if (bias == kBiasRelPos) return launch_variant<D, true, kBiasRelPos, kNormSoftmax, false>(p, stream);
-        return launch_variant<D, true, kBiasNone, kNormSoftmax, false>(p, stream);
+        if (bias == kBiasAlibi) return launch_variant<D, true, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
+        if (bias == kBiasRelPos) return launch_variant<D, true, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
+        return launch_variant<D, true, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
     }
-    if (bias == kBiasAlibi) return launch_variant<D, false, kBiasAlibi, kNormSoftmax, false>(p, stream);
-    if (bias == kBiasRelPos) return launch_variant<D, false, kBiasRelPos, kNormSoftmax, false>(p, stream);
-    return launch_variant<D, false, kBiasNone, kNormSoftmax, false>(p, stream);
+    if (bias == kBiasAlibi) return launch_variant<D, false, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
+    if (bias == kBiasRelPos) return launch_variant<D, false, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
+    return launch_variant<D, false, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
 }
 
 }  // namespace
 
 hipError_t launch_bf16_closed_form_d128(const AttnParams& p, hipStream_t stream)
 {
-    return launch_closed_form<128>(p, stream);
+    // a left-bounded band (sliding window) checks both bounds on partial tiles
+    return p.band.wl >= 0 ? launch_closed_form<128, true>(p, stream)
+                          : launch_closed_form<128, false>(p, stream);
 }
 
 hipError_t launch_bf16(const AttnParams& p, int head_dim, hipStream_t stream)

@@ -4,18 +4,28 @@
 
 namespace attn {
 
-hipError_t launch_bf16_closed_form_d64(const AttnParams& p, hipStream_t stream)
+namespace {
+
+template <bool LEFT>
+hipError_t closed_form_d64(const AttnParams& p, hipStream_t stream)
 {
     const bool sc = p.softcap > 0.0f;
     const int bias = p.slopes ? kBiasAlibi : (p.relpos ? kBiasRelPos : kBiasNone);
     if (sc) {
-        if (bias == kBiasAlibi) return launch_variant<64, true, kBiasAlibi, kNormSoftmax, false>(p, stream);
-        if (bias == kBiasRelPos) return launch_variant<64, true, kBiasRelPos, kNormSoftmax, false>(p, stream);
-        return launch_variant<64, true, kBiasNone, kNormSoftmax, false>(p, stream);
+        if (bias == kBiasAlibi) return launch_variant<64, true, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
+        if (bias == kBiasRelPos) return launch_variant<64, true, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
+        return launch_variant<64, true, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
     }
-    if (bias == kBiasAlibi) return launch_variant<64, false, kBiasAlibi, kNormSoftmax, false>(p, stream);
-    if (bias == kBiasRelPos) return launch_variant<64, false, kBiasRelPos, kNormSoftmax, false>(p, stream);
-    return launch_variant<64, false, kBiasNone, kNormSoftmax, false>(p, stream);
+    if (bias == kBiasAlibi) return launch_variant<64, false, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
+    if (bias == kBiasRelPos) return launch_variant<64, false, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
+    return launch_variant<64, false, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
+}
+
+}  // namespace
+
+hipError_t launch_bf16_closed_form_d64(const AttnParams& p, hipStream_t stream)
+{
+    return p.band.wl >= 0 ? closed_form_d64<true>(p, stream) : closed_form_d64<false>(p, stream);
 }
 
 }  // namespace attn

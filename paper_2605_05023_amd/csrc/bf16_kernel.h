@@ -72,13 +72,16 @@ constexpr int NT = 256;      // threads per workgroup (4 waves)
 constexpr float TAU = 8.0f;  // lazy-rescale threshold, log2 units
 
 // D: head dim; BN: keys per tile; SOFTCAP: soft-cap on; BIAS: kBias*;
-// NORM: kNorm*; GEN: per-row visible ranges (general mask path).
-template <int D_, int BN_, bool SOFTCAP_, int BIAS_, int NORM_, bool GEN_>
+// NORM: kNorm*; GEN: per-row visible ranges (general mask path); LEFT: the
+// band has a left bound (otherwise every row's first visible key is 0 and
+// partial tiles only check the right bound, which also masks keys past the
+// sequence end).
+template <int D_, int BN_, bool SOFTCAP_, int BIAS_, int NORM_, bool GEN_, bool LEFT_ = true>
 struct Traits {
     static constexpr int D = D_, BN = BN_;
     static constexpr bool SOFTCAP = SOFTCAP_, MODS = SOFTCAP_ || BIAS_ != kBiasNone;
     static constexpr int BIAS = BIAS_, NORM = NORM_;
-    static constexpr bool SOFTMAX = NORM_ == kNormSoftmax, GEN = GEN_;
+    static constexpr bool SOFTMAX = NORM_ == kNormSoftmax, GEN = GEN_, LEFT = LEFT_ || GEN_;
     static constexpr int NB = BN / 32;                   // 32-key blocks per tile
     static constexpr int ROWB = D * 2;                   // bytes per K/V row in LDS
     static constexpr int TILE = BN * ROWB;               // bytes per K or V tile
@@ -244,13 +247,29 @@ struct WaveState {
     float bias_abs, bias_lin;  // coefficients of |ip - j| and (jref - j), in units
 };
 
+// Visible-key bounds of this lane's row relative to the key of element
+// offset 0 in a tile (jn + 8 lh), so each element compares its compile-time
+// offset c = 32b + e + (e >= 8 ? 8 : 0) directly.
+struct MaskThr {
+    int lo, hi, pf;
+};
+
 template <class T>
-__device__ __forceinline__ bool visible(const WaveState<T>& ws, int j)
+__device__ __forceinline__ MaskThr mask_thresholds(const WaveState<T>& ws, int jn)
+{
+    const int base = jn + 8 * ws.lh;
+    return {ws.jlo - base, ws.jhi - base, ws.pfx - base};
+}
+
+template <class T>
+__device__ __forceinline__ bool visible(const MaskThr& m, int c)
 {
     if constexpr (T::GEN)
-        return j < ws.pfx || (j >= ws.jlo && j <= ws.jhi);
+        return c < m.pf || (c >= m.lo && c <= m.hi);
+    else if constexpr (T::LEFT)
+        return c >= m.lo && c <= m.hi;
     else
-        return j >= ws.jlo && j <= ws.jhi;
+        return c <= m.hi;
 }
 
 template <class T>
@@ -282,16 +301,18 @@ __device__ __forceinline__ float mods_and_max(f32x16 (&s)[T::NB], const AttnPara
                                               const WaveState<T>& ws, int j0)
 {
     float mx = -__builtin_inff();
+    const MaskThr mt = mask_thresholds(ws, j0);
 #pragma unroll
     for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            // element (b, e) is key j0 + 32b + 8lh + e + (e >= 8 ? 8 : 0)
-            int j = j0 + 32 * b + 8 * ws.lh + e + (e >= 8 ? 8 : 0);
+            // element (b, e) is key j0 + 8lh + c, c = 32b + e + (e >= 8 ? 8 : 0)
+            const int c = 32 * b + e + (e >= 8 ? 8 : 0);
+            const int j = j0 + 8 * ws.lh + c;
             float x = s[b][e];
             if constexpr (T::MODS) x = final_score<T>(x, p, ws, j);
             if constexpr (MASKED)
-                if (!visible<T>(ws, j)) x = -__builtin_inff();
+                if (!visible<T>(mt, c)) x = -__builtin_inff();
             s[b][e] = x;
             mx = __builtin_fmaxf(mx, x);
         }
@@ -450,6 +471,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
         __builtin_amdgcn_sched_barrier(0);
     });
     if constexpr (T::SOFTMAX) ws.l_run += rs;
+    const MaskThr mt = mask_thresholds(ws, jn);
     static_for<PV>([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = ic.value;
         constexpr int b = i / (2 * DBLK), u = (i / DBLK) % 2, d = i % DBLK;
@@ -461,12 +483,12 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
         if constexpr (i + PF < PV) read_v(i + PF);
         static_for<EP>([&](auto kc) __attribute__((always_inline)) {
             constexpr int el = i * EP + kc.value, bb = el / 16, e = el % 16;
-            // element (bb, e) is key jn + 32bb + 8lh + e + (e >= 8 ? 8 : 0)
-            const int j = jn + 32 * bb + 8 * ws.lh + e + (e >= 8 ? 8 : 0);
+            // element (bb, e) is key jn + 8lh + c, c = 32bb + e + (e >= 8 ? 8 : 0)
+            constexpr int c = 32 * bb + e + (e >= 8 ? 8 : 0);
             float x = sn[bb][e];
-            if constexpr (T::MODS) x = final_score<T>(x, p, ws, j);
+            if constexpr (T::MODS) x = final_score<T>(x, p, ws, jn + 8 * ws.lh + c);
             if constexpr (MASKED)
-                if (!visible<T>(ws, j)) x = -__builtin_inff();
+                if (!visible<T>(mt, c)) x = -__builtin_inff();
             sn[bb][e] = x;
             if constexpr (T::SOFTMAX) mx = __builtin_fmaxf(mx, x);
         });
@@ -862,10 +884,10 @@ constexpr int key_tile_width(int)
 #endif
 }
 
-template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN>
+template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN, bool LEFT = true>
 hipError_t launch_variant(const AttnParams& p, hipStream_t stream)
 {
-    using T = Traits<D, key_tile_width(D), SOFTCAP, BIAS, NORM, GEN>;
+    using T = Traits<D, key_tile_width(D), SOFTCAP, BIAS, NORM, GEN, LEFT>;
     int64_t blocks = (int64_t)p.num_q_tiles * p.hq * p.batch;
     hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)blocks), dim3(NT), 0, stream, p);
     return hipGetLastError();
