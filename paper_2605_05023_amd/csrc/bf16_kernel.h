@@ -205,7 +205,11 @@ struct Bool {
 // Map the hardware workgroup id to (sequence, query head, query tile).
 // Query tiles are issued longest-first: the last tiles of a causal sequence
 // see the most keys, so the order is descending unless the host asks for
-// ascending (q_order = 1: the first tiles are the heaviest, e.g. global rows). Mode 1 keeps all query heads of a kv-head group on one
+// ascending (q_order = 1: the first tiles are the heaviest, e.g. global rows).
+// Within an XCD the kv-head groups are taken `chunk` at a time (every query
+// head and query tile of the chunk, longest-first inside it), so the K/V
+// tiles in use at any moment belong to a few groups and stay in that XCD's
+// L2 instead of cycling every group's K/V through the caches once per tile. Mode 1 keeps all query heads of a kv-head group on one
 // XCD (workgroup ids are dealt round-robin over the 8 XCDs), so their K/V
 // tiles are shared through that XCD's L2.
 __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
@@ -215,9 +219,12 @@ __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
     if (p.map_mode == 1) {
         int x = w & 7, k = w >> 3;
         int groups_per_xcd = (p.batch * p.hkv) >> 3;
-        int per_tile = groups_per_xcd * p.group;
-        int qt_rev = k / per_tile, rem = k % per_tile;
-        int gi = rem / p.group, r = rem % p.group;
+        int chunk_items = p.chunk * p.group * p.num_q_tiles;
+        int c = k / chunk_items;
+        int cg = min(p.chunk, groups_per_xcd - c * p.chunk);  // groups in this chunk
+        int rem = k - c * chunk_items;
+        int qt_rev = rem / (cg * p.group), r2 = rem % (cg * p.group);
+        int gi = c * p.chunk + r2 / p.group, r = r2 % p.group;
         int g = x + 8 * gi;
         it.b = g / p.hkv;
         it.hq = (g % p.hkv) * p.group + r;

@@ -21,6 +21,7 @@ struct AttnParams {
     int32_t num_q_tiles;     // ceil(max query length / block_m)
     int32_t map_mode;        // workgroup order (0 natural, 1 kv-group per XCD)
     int32_t q_order;         // query tiles issued 0 last-first (causal-like), 1 first-first
+    int32_t chunk;           // map_mode 1: kv-head groups per chunk within an XCD
     int64_t total_q;         // varlen: rows of the [Hq, total_q] LSE
     // element strides
     int64_t sq_b, sq_h, sq_s;

@@ -137,3 +137,27 @@ def test_workload_full_size(name):
     else:
         rows = sample_rows(inp, n_random=768, seed=wl.seed)
     assert_parity(inp, o, lse, rows=rows, label=name)
+
+
+# Workgroup order: when K/V exceed the cache, the kv-head groups of each XCD
+# are walked in chunks. A large-batch causal shape (537 MB of K/V) takes that
+# order by itself; small shapes force odd chunk sizes (including a partial
+# last chunk: 3 groups per XCD in chunks of 2) through ATTN_CHUNK.
+def test_chunked_order_large_batch():
+    wl = W("causal_b16_h32_s2048", "bf16", 16, 32, 32, 2048, 128, CAUSAL, seed=13)
+    inp = make_inputs(wl)
+    rows = sample_rows(inp, 512, seed=5)
+    log(f"[chunked] {wl.name}: {len(rows)} sampled rows")
+    o, lse = run_gpu(inp)
+    assert_parity(inp, o, lse, rows=rows, label=wl.name)
+
+
+@pytest.mark.parametrize("chunk", ["1", "2", "3"])
+def test_chunked_order_forced(chunk, monkeypatch):
+    monkeypatch.setenv("ATTN_CHUNK", chunk)
+    for wl in (W("chunk_mha", "bf16", 2, 12, 12, 300, 128, CAUSAL, seed=14),
+               W("chunk_gqa", "bf16", 3, 16, 8, 260, 64, WINDOW, 60, 0, seed=15)):
+        inp = make_inputs(wl)
+        log(f"[chunked] {wl.name} chunk={chunk}")
+        o, lse = run_gpu(inp)
+        assert_parity(inp, o, lse, label=f"{wl.name} chunk {chunk}")
