@@ -2,9 +2,11 @@
 //
 // fp32 has no faster matrix path on this chip (the fp32 matrix and vector
 // peaks are equal), so each lane owns one query row and accumulates with
-// fp32 vector FMAs. A workgroup is one 64-lane wavefront covering 64 query
-// rows of one (sequence, query head); key/value tiles of 32 keys are staged
-// through LDS and read as broadcasts. The score modifications, the masks with
+// fp32 vector FMAs. A workgroup covers 64 query rows of one (sequence, query
+// head) with four wavefronts that split the key tiles between them (wave w
+// takes tiles lo + w, lo + w + 4, ...), each staging its own key/value tiles
+// through LDS and reading them as broadcasts; the four partial results
+// (running max, sum and O per row) are merged through LDS at the end. The score modifications, the masks with
 // tile skipping, the base-2 online softmax and the ReLU / Sigmoid
 // normalisations are the same as in the bf16 kernel (Eq. 1 and 2 of Section
 // 2.2, Appendix A). On the general mask path each lane derives its row's
@@ -22,9 +24,12 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 64;  // query rows per workgroup (one per lane)
-constexpr int BN = 32;  // keys per tile
-constexpr int NT = 64;
+constexpr int BM = 64;     // query rows per workgroup (one per lane of every wave)
+constexpr int NW = 4;      // wavefronts, each with a share of the key tiles
+constexpr int NT = 64 * NW;
+
+// Keys per tile: the four waves' double K/V tiles fit 64 KiB of LDS.
+constexpr int key_tile(int d) { return d == 128 ? 16 : 32; }
 
 __device__ __forceinline__ int wave_min(int x)
 {
@@ -44,11 +49,14 @@ template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN>
 __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
 {
     constexpr bool SOFTMAX = NORM == kNormSoftmax;
+    constexpr int BN = key_tile(D);
+    constexpr int KV_BYTES = NW * 2 * BN * D * 4;         // per-wave K and V tiles
+    constexpr int MERGE_BYTES = 2 * BM * (D + 2) * 4;      // two partial results
     __shared__ __attribute__((aligned(16))) float qs[BM][D + 4];  // padded rows
-    __shared__ __attribute__((aligned(16))) float ks[BN][D];
-    __shared__ __attribute__((aligned(16))) float vs[BN][D];
+    __shared__ __attribute__((aligned(16))) char lds[KV_BYTES > MERGE_BYTES ? KV_BYTES : MERGE_BYTES];
 
     const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int nbh = p.batch * p.hq;
     const int w = blockIdx.x;
     const int qt = p.q_order ? w / nbh : p.num_q_tiles - 1 - w / nbh;
@@ -66,7 +74,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
         lk = p.seqlen_k;
     }
     const int q0 = qt * BM;
-    if (q0 >= lq) return;
+    if (q0 >= lq) return;  // whole workgroup
     const int hkv = hq / p.group;
     const float* qb = static_cast<const float*>(p.q);
     const float* kb = static_cast<const float*>(p.k);
@@ -85,16 +93,16 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
         voff = (int64_t)b * p.sv_b + (int64_t)hkv * p.sv_h;
     }
 
-    const int qi = q0 + tid;
-    {
-        const float* src = qb + qoff + (int64_t)qi * p.sq_s;
-#pragma unroll
-        for (int c = 0; c < D / 4; ++c) {
-            f32x4 x = {0.f, 0.f, 0.f, 0.f};
-            if (qi < lq) x = *reinterpret_cast<const f32x4*>(src + 4 * c);
-            *reinterpret_cast<f32x4*>(&qs[tid][4 * c]) = x;
-        }
+    // Q rows into LDS, all four waves cooperating.
+    for (int e = tid; e < BM * (D / 4); e += NT) {
+        const int r = e / (D / 4), c = e % (D / 4);
+        f32x4 x = {0.f, 0.f, 0.f, 0.f};
+        if (q0 + r < lq) x = *reinterpret_cast<const f32x4*>(qb + qoff + (int64_t)(q0 + r) * p.sq_s + 4 * c);
+        *reinterpret_cast<f32x4*>(&qs[r][4 * c]) = x;
     }
+    __syncthreads();
+
+    const int qi = q0 + lane;  // every wave covers the same 64 rows
     RowVis rv = {0, 1, 0};
     int t_lo, t_hi;  // key tiles visited
     if constexpr (GEN) {
@@ -127,12 +135,16 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     for (int d = 0; d < D; ++d) o[d] = 0.0f;
     float m_run = -__builtin_inff(), l_run = 0.0f;
 
-    for (int kt = t_lo; kt < t_hi; ++kt) {
+    // This wave's K and V tiles; only this wave touches them, so ordering its
+    // own LDS writes and reads needs a fence, not a workgroup barrier.
+    float (*ks)[D] = reinterpret_cast<float (*)[D]>(lds + wave * 2 * BN * D * 4);
+    float (*vs)[D] = reinterpret_cast<float (*)[D]>(lds + (wave * 2 + 1) * BN * D * 4);
+    for (int kt = t_lo + wave; kt < t_hi; kt += NW) {
         const int j0 = kt * BN;
-        __syncthreads();  // previous tile fully consumed
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // previous tile fully read
 #pragma unroll
-        for (int i = 0; i < BN * D / 4 / NT; ++i) {
-            int e = i * NT + tid;
+        for (int i = 0; i < BN * D / 4 / 64; ++i) {
+            int e = i * 64 + lane;
             int r = e / (D / 4), c = e % (D / 4);
             f32x4 kx = {0.f, 0.f, 0.f, 0.f}, vx = {0.f, 0.f, 0.f, 0.f};
             if (j0 + r < lk) {
@@ -142,7 +154,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
             *reinterpret_cast<f32x4*>(&ks[r][4 * c]) = kx;
             *reinterpret_cast<f32x4*>(&vs[r][4 * c]) = vx;
         }
-        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // tile written
         const bool band_hit = rv.jlo <= rv.jhi && rv.jhi >= j0 && rv.jlo <= j0 + BN - 1;
         if (!band_hit && j0 >= rv.pfx) continue;  // row sees none of the tile
         const bool full = j0 + BN <= rv.pfx || (rv.jlo <= j0 && j0 + BN - 1 <= rv.jhi);
@@ -151,7 +163,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
         for (int j = 0; j < BN; ++j) s[j] = 0.0f;
 #pragma unroll
         for (int c = 0; c < D / 4; ++c) {
-            f32x4 qx = *reinterpret_cast<const f32x4*>(&qs[tid][4 * c]);
+            f32x4 qx = *reinterpret_cast<const f32x4*>(&qs[lane][4 * c]);
 #pragma unroll
             for (int j = 0; j < BN; ++j) {
                 f32x4 kx = *reinterpret_cast<const f32x4*>(&ks[j][4 * c]);
@@ -171,31 +183,24 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
             s[j] = x;
             mx = __builtin_fmaxf(mx, x);
         }
-        if constexpr (!SOFTMAX) {  // O += act(S) V; the 1/L comes at the end
+        float alpha = 1.0f, m_new = m_run;
+        if constexpr (SOFTMAX) {
+            m_new = __builtin_fmaxf(m_run, mx);
+            alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 when m_run = -inf
+            m_run = m_new;
+            l_run *= alpha;
 #pragma unroll
-            for (int j = 0; j < BN; ++j) {
-                float pe = activation<NORM>(s[j]);
-#pragma unroll
-                for (int c = 0; c < D / 4; ++c) {
-                    f32x4 vx = *reinterpret_cast<const f32x4*>(&vs[j][4 * c]);
-                    o[4 * c + 0] = __builtin_fmaf(pe, vx[0], o[4 * c + 0]);
-                    o[4 * c + 1] = __builtin_fmaf(pe, vx[1], o[4 * c + 1]);
-                    o[4 * c + 2] = __builtin_fmaf(pe, vx[2], o[4 * c + 2]);
-                    o[4 * c + 3] = __builtin_fmaf(pe, vx[3], o[4 * c + 3]);
-                }
-            }
-            continue;
+            for (int d = 0; d < D; ++d) o[d] *= alpha;
         }
-        const float m_new = __builtin_fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 when m_run = -inf
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int d = 0; d < D; ++d) o[d] *= alpha;
 #pragma unroll
         for (int j = 0; j < BN; ++j) {
-            float pe = __builtin_amdgcn_exp2f(s[j] - m_new);
-            l_run += pe;
+            float pe;
+            if constexpr (SOFTMAX) {
+                pe = __builtin_amdgcn_exp2f(s[j] - m_new);
+                l_run += pe;
+            } else {
+                pe = activation<NORM>(s[j]);  // the 1/L comes at the end
+            }
 #pragma unroll
             for (int c = 0; c < D / 4; ++c) {
                 f32x4 vx = *reinterpret_cast<const f32x4*>(&vs[j][4 * c]);
@@ -206,6 +211,44 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
             }
         }
     }
+
+    // Merge the four partial results: waves 1 and 3 into 0 and 2, then 2 into 0.
+    // A partial (m, l, O) with m = -inf saw no key and contributes nothing.
+    float* mb = reinterpret_cast<float*>(lds);
+    auto publish = [&](int slot) {
+        float* row = mb + (slot * BM + lane) * (D + 2);
+#pragma unroll
+        for (int d = 0; d < D; ++d) row[d] = o[d];
+        row[D] = m_run;
+        row[D + 1] = l_run;
+    };
+    auto absorb = [&](int slot) {
+        const float* row = mb + (slot * BM + lane) * (D + 2);
+        if constexpr (SOFTMAX) {
+            const float m_o = row[D], l_o = row[D + 1];
+            const float m_new = __builtin_fmaxf(m_run, m_o);
+            const float a = m_run == -__builtin_inff() ? 0.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+            const float c = m_o == -__builtin_inff() ? 0.0f : __builtin_amdgcn_exp2f(m_o - m_new);
+            m_run = m_new;
+            l_run = a * l_run + c * l_o;
+#pragma unroll
+            for (int d = 0; d < D; ++d) o[d] = a * o[d] + c * row[d];
+        } else {
+#pragma unroll
+            for (int d = 0; d < D; ++d) o[d] += row[d];
+        }
+    };
+    __syncthreads();  // every wave is done with its K/V tiles
+    if (wave == 1) publish(0);
+    if (wave == 3) publish(1);
+    __syncthreads();
+    if (wave == 0) absorb(0);
+    if (wave == 2) absorb(1);
+    __syncthreads();
+    if (wave == 2) publish(0);
+    __syncthreads();
+    if (wave != 0) return;
+    absorb(0);
 
     if (qi < lq) {
         float inv;
