@@ -27,26 +27,19 @@ enum : int {
 // Normalisation selected at compile time.
 enum : int { kNormSoftmax = 0, kNormRelu = 1, kNormSigmoid = 2 };
 
-// tanh for fp32 with small absolute and relative error over the whole line.
-// |x| < 0.4: Taylor series of tanh about 0 (coefficients from the Bernoulli
-// numbers, 2^{2n}(2^{2n}-1)B_{2n}/(2n)!) through x^13; the first dropped term
-// is below 2e-9 there. |x| >= 0.4: tanh|x| = (1 - e)/(1 + e) with
-// e = exp(-2|x|) <= 0.45, so the subtraction loses no significant bits.
+// tanh for fp32 with small relative error over the whole line (<= ~2e-6,
+// so the soft-capped score C tanh(s/C) keeps a relative error of that order
+// whatever C is). |x| < 1/16: x - x^3/3 (the first dropped term, 2x^5/15, is
+// below 2.1e-6 x there). Elsewhere, for either sign, 1 - 2/(1 + e^(2x)):
+// with |tanh x| >= 0.0624 its absolute error (about 2e-7 from the exp and
+// reciprocal) is below 3.3e-6 relative; it tends to +-1 without overflow.
 __device__ __forceinline__ float tanh_f32(float x)
 {
-    float ax = __builtin_fabsf(x);
-    float x2 = x * x;
-    float poly = 21844.0f / 6081075.0f;
-    poly = __builtin_fmaf(poly, x2, -1382.0f / 155925.0f);
-    poly = __builtin_fmaf(poly, x2, 62.0f / 2835.0f);
-    poly = __builtin_fmaf(poly, x2, -17.0f / 315.0f);
-    poly = __builtin_fmaf(poly, x2, 2.0f / 15.0f);
-    poly = __builtin_fmaf(poly, x2, -1.0f / 3.0f);
-    float small = __builtin_fmaf(ax * x2, poly, ax);
-    float e = __builtin_amdgcn_exp2f(-2.0f * kLog2e * ax);
-    float big = (1.0f - e) * __builtin_amdgcn_rcpf(1.0f + e);
-    float r = ax < 0.4f ? small : big;
-    return __builtin_copysignf(r, x);
+    const float x2 = x * x;
+    const float cubic = __builtin_fmaf(x2 * x, -1.0f / 3.0f, x);
+    const float e = __builtin_amdgcn_exp2f(x * (2.0f * kLog2e));
+    const float t = __builtin_fmaf(-2.0f, __builtin_amdgcn_rcpf(1.0f + e), 1.0f);
+    return __builtin_fabsf(x) < 0.0625f ? cubic : t;
 }
 
 // Final score, in units, of a raw dot product `dot` for the query at key-axis
