@@ -432,7 +432,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     constexpr int NB = T::NB, DBLK = T::DBLK;
     constexpr int QK = T::KSTEPS * NB;   // QK^T MFMAs (t-major, block-minor)
     constexpr int PV = 2 * NB * DBLK;    // P V MFMAs (b, u, d)
-    constexpr int PF = 2;                // read prefetch distance in slices
+    constexpr int PF = 3;                // read prefetch distance in slices
     constexpr int EQ = 16 * NB / QK;     // exponentials per QK slice
     constexpr int EP = 16 * NB / PV;     // score elements per P V slice
     static_assert(EQ % 2 == 0 && EQ * QK == 16 * NB && EP * PV == 16 * NB, "slice split");
