@@ -138,6 +138,15 @@ __device__ __forceinline__ uint32_t load_lane_offset(int wave, int lane, int64_t
 // it read as zero). The row offset is wave-uniform and added to the lane's
 // constant byte offset.
 template <class T>
+__device__ __forceinline__ void issue_load(char* lds_tile, __amdgpu_buffer_rsrc_t rs, int j0,
+                                           uint32_t row_bytes, uint32_t lane_off, int wave, int p)
+{
+    const uint32_t off = lane_off + (uint32_t)(j0 + p * T::ROWS_PER_LOAD) * row_bytes;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rs, (lds_void*)(lds_tile + (4 * p + wave) * 1024), 16, off, 0, 0, 0);
+}
+
+template <class T>
 __device__ __forceinline__ void issue_tile(char* lds_tile, __amdgpu_buffer_rsrc_t rs, int j0,
                                            uint32_t row_bytes, uint32_t lane_off, int wave)
 {
@@ -292,9 +301,9 @@ template <class T>
 __device__ __forceinline__ void qk_tile(const char* kt, const WaveState<T>& ws, f32x16 (&s)[T::NB])
 {
 #pragma unroll
-    for (int t = 0; t < T::KSTEPS; ++t) {
+    for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
-        for (int b = 0; b < T::NB; ++b) {
+        for (int t = 0; t < T::KSTEPS; ++t) {
             bf16x8 a = *reinterpret_cast<const bf16x8*>(kt + 32 * b * T::ROWB + ws.kaddr[t]);
             s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ws.qf[t], t == 0 ? f32x16{} : s[b], 0,
                                                            0, 0);
@@ -417,20 +426,29 @@ __device__ __forceinline__ void pv_tile(const char* vt, const u32x4 (&pw)[T::NB]
 }
 
 // One pipelined step, written out as explicit slices. Each QK^T slice issues
-// one MFMA of S_next = Q K_next^T, the K read of the MFMA PF slices later and
-// an equal share of the exponentials of the current tile (P and row sum);
-// each P V slice issues one MFMA of O^T += V^T P^T, the two transpose reads
-// of a later MFMA and a share of the score mods, mask and max of S_next. A
-// scheduling barrier after every slice keeps this order, so the vector work
-// runs while the matrix cores are busy and LDS latency stays hidden.
-template <class T, bool MASKED>
+// one MFMA of S_next = Q K_next^T, the K read of the MFMA PF slices later, an
+// equal share of the exponentials of the current tile (P and row sum) and,
+// in the first slices, one of the global->LDS loads of the tiles the next
+// step reads (`load(i)`, i < 2 LOADS), whose issue then overlaps the matrix
+// products; each P V slice issues one MFMA of O^T += V^T P^T, the two
+// transpose reads of a later MFMA and a share of the score mods, mask and max
+// of S_next. A scheduling barrier after every slice keeps this order, so the
+// vector work runs while the matrix cores are busy and LDS latency stays
+// hidden. The QK^T products run block by block: each accumulation chain is
+// issued back to back (a product that depends on the one just before it
+// issues without waiting for its result, one that depends on the one two
+// before stalls).
+template <class T, bool MASKED, class LOADER>
 __device__ __forceinline__ void pipelined_step(const char* kread, const char* vread,
                                                WaveState<T>& ws, const f32x16 (&sc)[T::NB],
                                                f32x16 (&sn)[T::NB], const AttnParams& p,
-                                               float m_use, int jn)
+                                               float m_use, int jn, LOADER&& load)
 {
     constexpr int NB = T::NB, DBLK = T::DBLK;
-    constexpr int QK = T::KSTEPS * NB;   // QK^T MFMAs (t-major, block-minor)
+    constexpr int QK = T::KSTEPS * NB;   // QK^T MFMAs (block-major, k-step-minor)
+    constexpr int NLD = 2 * T::LOADS;    // loads of the next step's K and V tiles
+    constexpr int LSTEP = QK / NLD;      // one load every LSTEP slices
+    static_assert(LSTEP >= 1 && LSTEP * NLD == QK, "load split");
     constexpr int PV = 2 * NB * DBLK;    // P V MFMAs (b, u, d)
     constexpr int PF = 3;                // read prefetch distance in slices
     constexpr int EQ = 16 * NB / QK;     // exponentials per QK slice
@@ -443,7 +461,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     float rs = 0.0f, mx = -__builtin_inff();
 
     auto read_k = [&](int i) __attribute__((always_inline)) {
-        const int t = i / NB, b = i % NB;
+        const int b = i / T::KSTEPS, t = i % T::KSTEPS;
         kop[i] = *reinterpret_cast<const bf16x8*>(kread + 32 * b * T::ROWB + ws.kaddr[t]);
     };
     auto read_v = [&](int i) __attribute__((always_inline)) {
@@ -456,7 +474,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     static_for<PF>([&](auto ic) __attribute__((always_inline)) { read_k(ic.value); });
     __builtin_amdgcn_sched_barrier(0);
     static_for<QK>([&](auto ic) __attribute__((always_inline)) {
-        constexpr int i = ic.value, t = i / NB, b = i % NB;
+        constexpr int i = ic.value, b = i / T::KSTEPS, t = i % T::KSTEPS;
         if constexpr (t == 0)
             sn[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[i], ws.qf[t], f32x16{}, 0, 0, 0);
         else
@@ -465,6 +483,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             read_k(i + PF);
         else
             read_v(i + PF - QK);
+        if constexpr (i % LSTEP == 0) load(i / LSTEP);
         static_for<EQ / 2>([&](auto kc) __attribute__((always_inline)) {
             constexpr int el = i * EQ + 2 * kc.value, bb = el / 16, e = el % 16;
             const float p0 = norm_value<T>(sc[bb][e], m_use, p.scale_u);
@@ -780,13 +799,19 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             char* vwrite = PAR ? lds_v0 : lds_v1;
             rescale_if_needed(ws);
             const int t1 = tile_of(j + 1);
-            if (j + 2 < jend) issue_tile<T>(kwrite, krs, tile_of(j + 2) * BN, krow, klp, wave);
-            issue_tile<T>(vwrite, vrs, t1 * BN, vrow, vlp, wave);
+            // past the last tile the K load reads rows beyond the sequence end (zeros)
+            const int jk = j + 2 < jend ? tile_of(j + 2) * BN : lk;
+            auto load = [&](int i) __attribute__((always_inline)) {
+                if (i < T::LOADS)
+                    issue_load<T>(kwrite, krs, jk, krow, klp, wave, i);
+                else
+                    issue_load<T>(vwrite, vrs, t1 * BN, vrow, vlp, wave, i - T::LOADS);
+            };
             const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
             if constexpr (PAR == 0)
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, t1 * BN);
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, t1 * BN, load);
             else
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, t1 * BN);
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, t1 * BN, load);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
         };
