@@ -69,7 +69,17 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int BM = 128;      // query rows per workgroup
 constexpr int NT = 256;      // threads per workgroup (4 waves)
-constexpr float TAU = 8.0f;  // lazy-rescale threshold, log2 units
+// Softmax with score mods keeps a lazily updated running max: it moves only
+// when a tile's max exceeds it by more than TAU (log2 units), so P <= 2^TAU.
+constexpr float TAU = 8.0f;
+// Softmax without score mods and without a left bound on the visible keys
+// (so that a row's first tile is the workgroup's first tile, whose max sets
+// the running max) does without the tile max on the common path:
+// the exponentials of a tile use the running max as it stands, and a tile
+// whose per-lane partial sums of P all stay within PSUM_BOUND = 2^TAU keeps
+// every P <= 2^TAU as above (a larger bound would leave the dominant P further
+// from 1, where its bf16 rounding enters O unmatched by the fp32 row sum).
+constexpr float PSUM_BOUND = 256.0f;
 
 // D: head dim; BN: keys per tile; SOFTCAP: soft-cap on; BIAS: kBias*;
 // NORM: kNorm*; GEN: per-row visible ranges (general mask path); LEFT: the
@@ -82,6 +92,9 @@ struct Traits {
     static constexpr bool SOFTCAP = SOFTCAP_, MODS = SOFTCAP_ || BIAS_ != kBiasNone;
     static constexpr int BIAS = BIAS_, NORM = NORM_;
     static constexpr bool SOFTMAX = NORM_ == kNormSoftmax, GEN = GEN_, LEFT = LEFT_ || GEN_;
+    // softmax without score mods whose rows all see the first visited tile
+    // (no left bound): running max checked through the row sums
+    static constexpr bool MAXFREE = SOFTMAX && !MODS && !LEFT;
     static constexpr int NB = BN / 32;                   // 32-key blocks per tile
     static constexpr int ROWB = D * 2;                   // bytes per K/V row in LDS
     static constexpr int TILE = BN * ROWB;               // bytes per K or V tile
@@ -255,8 +268,9 @@ struct WaveState {
     int vaddr[T::DBLK][2];     // LDS byte offsets of this lane's V transpose reads
     f32x16 oacc[T::DBLK];      // O^T accumulator
     f32x16 sa[T::NB], sb[T::NB];  // scores of tiles of even / odd parity
-    float m_run, l_run, alpha;    // softmax only
-    bool need;
+    float m_run, l_run;           // softmax only: running max (units) and partial row sum
+    float alpha;                  // softmax with mods: rescale factor of O and l
+    bool need;                    // softmax with mods: O and l must be rescaled
     // row constants: visible keys j < pfx (general path) and jlo <= j <= jhi;
     // key-axis position ip; relative-position reference jref
     int lh, pfx, jlo, jhi, ip, jref;
@@ -339,31 +353,6 @@ __device__ __forceinline__ float mods_and_max(f32x16 (&s)[T::NB], const AttnPara
     return mx;
 }
 
-// Fold a tile max into the running max; decide whether O must be rescaled
-// (only when the max grew by more than TAU, so exp2 arguments stay <= TAU).
-template <class T>
-__device__ __forceinline__ void update_max(WaveState<T>& ws, float mx)
-{
-    if constexpr (!T::SOFTMAX) return;
-    const float m_new = __builtin_fmaxf(ws.m_run, mx);
-    ws.need = m_new > ws.m_run + TAU;
-    ws.alpha = ws.need ? __builtin_amdgcn_exp2f(ws.m_run - m_new) : 1.0f;
-    if (ws.need) ws.m_run = m_new;
-}
-
-template <class T>
-__device__ __forceinline__ void rescale_if_needed(WaveState<T>& ws)
-{
-    if constexpr (!T::SOFTMAX) return;
-    if (__builtin_amdgcn_ballot_w64(ws.need)) {
-        ws.l_run *= ws.alpha;
-#pragma unroll
-        for (int d = 0; d < T::DBLK; ++d)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) ws.oacc[d][e] *= ws.alpha;
-    }
-}
-
 // Norm of one score (in units; raw dot product when there are no mods):
 // softmax exp2(S - m), or the ReLU / Sigmoid activation of the natural score.
 template <class T>
@@ -376,10 +365,45 @@ __device__ __forceinline__ float norm_value(float x, float m_use, float scale_u)
     }
 }
 
-// P = Norm(S) as bf16 B operands of the P V product, plus (softmax) the row sum.
+// Softmax with mods: fold a tile max into the running max; decide whether O
+// must be rescaled (only when the max grew by more than TAU).
 template <class T>
-__device__ __forceinline__ void exp_tile(f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2], float m_use,
-                                         float scale_u, float& l_run)
+__device__ __forceinline__ void update_max(WaveState<T>& ws, float mx)
+{
+    if constexpr (!T::SOFTMAX || T::MAXFREE) return;
+    const float m_new = __builtin_fmaxf(ws.m_run, mx);
+    ws.need = m_new > ws.m_run + TAU;
+    ws.alpha = ws.need ? __builtin_amdgcn_exp2f(ws.m_run - m_new) : 1.0f;
+    if (ws.need) ws.m_run = m_new;
+}
+
+template <class T>
+__device__ __forceinline__ void rescale_if_needed(WaveState<T>& ws)
+{
+    if constexpr (!T::SOFTMAX || T::MAXFREE) return;
+    if (__builtin_amdgcn_ballot_w64(ws.need)) {
+        ws.l_run *= ws.alpha;
+#pragma unroll
+        for (int d = 0; d < T::DBLK; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) ws.oacc[d][e] *= ws.alpha;
+    }
+}
+
+// Does the row of this lane see a key of the tile starting at key jc?
+template <class T>
+__device__ __forceinline__ bool row_sees_tile(const WaveState<T>& ws, int jc)
+{
+    const bool band = ws.jlo <= ws.jhi && ws.jlo <= jc + T::BN - 1 && ws.jhi >= jc;
+    if constexpr (T::GEN) return band || ws.pfx > jc;
+    return band;
+}
+
+// P = Norm(S) as bf16 B operands of the P V product; returns (softmax) this
+// lane's partial row sum.
+template <class T>
+__device__ __forceinline__ float exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2],
+                                          float m_use, float scale_u)
 {
     float rs = 0.0f;
 #pragma unroll
@@ -398,7 +422,53 @@ __device__ __forceinline__ void exp_tile(f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][
             }
         }
     }
-    if constexpr (T::SOFTMAX) l_run += rs;
+    return rs;
+}
+
+// After the exponentials of tile j (first key jc) the row sums join l. With
+// MAXFREE the exponentials were made with the running max as it stands (0
+// while a row has seen no key): P is kept when every lane's partial sum stays
+// within PSUM_BOUND and no row sees its first keys in this tile. Otherwise
+// (rare: the first keys of a row whose first tile this is not, a jump of the
+// max) the running max of the affected rows moves to the max over the tile's
+// scores, O and l are rescaled, and P and the row sums are recomputed from
+// the scores. The two lanes of a row take the same decision. The row max
+// then plays no part in the common path, which saves its reductions on every
+// tile.
+template <class T>
+__device__ __forceinline__ void check_tile(WaveState<T>& ws, const f32x16 (&s)[T::NB],
+                                           u32x4 (&pw)[T::NB][2], float rs, const AttnParams& p,
+                                           int jc)
+{
+    if constexpr (!T::SOFTMAX) return;
+    if constexpr (!T::MAXFREE) {
+        ws.l_run += rs;
+        return;
+    }
+    bool need = rs > PSUM_BOUND;
+    if (ws.m_run == -__builtin_inff()) need = need || row_sees_tile(ws, jc);
+    if (__builtin_amdgcn_ballot_w64(need)) {
+        const bool need_row = pair_max(need ? 1.0f : 0.0f) > 0.0f;
+        float tm = -__builtin_inff();
+#pragma unroll
+        for (int b = 0; b < T::NB; ++b)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) tm = __builtin_fmaxf(tm, s[b][e]);
+        tm = pair_max(tm);
+        if constexpr (!T::MODS) tm *= p.scale_u;  // raw max -> units (scale > 0)
+        const float m_old = ws.m_run;
+        const float m_new = need_row ? __builtin_fmaxf(m_old, tm) : m_old;
+        const float alpha =
+            need_row && m_old != -__builtin_inff() ? __builtin_amdgcn_exp2f(m_old - m_new) : 1.0f;
+        ws.m_run = m_new;
+        ws.l_run *= alpha;
+#pragma unroll
+        for (int d = 0; d < T::DBLK; ++d)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) ws.oacc[d][e] *= alpha;
+        rs = exp_tile<T>(s, pw, m_new == -__builtin_inff() ? 0.0f : m_new, p.scale_u);
+    }
+    ws.l_run += rs;
 }
 
 // O^T += V^T P^T for the V tile in LDS at `vt`.
@@ -442,7 +512,7 @@ template <class T, bool MASKED, class LOADER>
 __device__ __forceinline__ void pipelined_step(const char* kread, const char* vread,
                                                WaveState<T>& ws, const f32x16 (&sc)[T::NB],
                                                f32x16 (&sn)[T::NB], const AttnParams& p,
-                                               float m_use, int jn, LOADER&& load)
+                                               float m_use, int jc, int jn, LOADER&& load)
 {
     constexpr int NB = T::NB, DBLK = T::DBLK;
     constexpr int QK = T::KSTEPS * NB;   // QK^T MFMAs (block-major, k-step-minor)
@@ -496,7 +566,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
         });
         __builtin_amdgcn_sched_barrier(0);
     });
-    if constexpr (T::SOFTMAX) ws.l_run += rs;
+    check_tile<T>(ws, sc, pw, rs, p, jc);
     const MaskThr mt = mask_thresholds(ws, jn);
     static_for<PV>([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = ic.value;
@@ -516,11 +586,11 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             if constexpr (MASKED)
                 if (!visible<T>(mt, c)) x = -__builtin_inff();
             sn[bb][e] = x;
-            if constexpr (T::SOFTMAX) mx = __builtin_fmaxf(mx, x);
+            if constexpr (T::SOFTMAX && !T::MAXFREE) mx = __builtin_fmaxf(mx, x);
         });
         __builtin_amdgcn_sched_barrier(0);
     });
-    if constexpr (T::SOFTMAX) {
+    if constexpr (T::SOFTMAX && !T::MAXFREE) {
         mx = pair_max(mx);
         if constexpr (!T::MODS) mx *= p.scale_u;  // raw max -> log2 units (scale > 0)
         update_max(ws, mx);
@@ -530,10 +600,11 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
 // The last step of the key loop: exponentials and P V of the current tile.
 template <class T>
 __device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, f32x16 (&sc)[T::NB],
-                                          const AttnParams& p, float m_use)
+                                          const AttnParams& p, float m_use, int jc)
 {
     u32x4 pw[T::NB][2];
-    exp_tile<T>(sc, pw, m_use, p.scale_u, ws.l_run);
+    const float rs = exp_tile<T>(sc, pw, m_use, p.scale_u);
+    check_tile<T>(ws, sc, pw, rs, p, jc);
     pv_tile<T>(vread, pw, ws);
 }
 
@@ -781,9 +852,14 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             masked_lo = !gen_full(t0);
         else
             masked_lo = !(t0 >= gp.full_lo && t0 < gp.full_hi);
-        float mx = masked_lo ? mods_and_max<T, true>(ws.sa, p, ws, t0 * BN)
-                             : mods_and_max<T, false>(ws.sa, p, ws, t0 * BN);
-        update_max(ws, mx);
+        // the running max starts at the first tile's max (-inf for rows that
+        // see none of its keys)
+        const float mx = masked_lo ? mods_and_max<T, true>(ws.sa, p, ws, t0 * BN)
+                                   : mods_and_max<T, false>(ws.sa, p, ws, t0 * BN);
+        if constexpr (T::MAXFREE)
+            ws.m_run = mx;
+        else
+            update_max(ws, mx);
         __syncthreads();  // K buffer 0 is reloaded in the first iteration
 
         // Iteration j with parity PAR = (j - jbeg) & 1 reads K_{j+1} from K
@@ -809,9 +885,11 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             };
             const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
             if constexpr (PAR == 0)
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, t1 * BN, load);
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, tile_of(j) * BN,
+                                          t1 * BN, load);
             else
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, t1 * BN, load);
+                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, tile_of(j) * BN,
+                                          t1 * BN, load);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
         };
@@ -860,9 +938,9 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         rescale_if_needed(ws);
         const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
         if (par)
-            last_step<T>(lds_v1, ws, ws.sb, p, m_use);
+            last_step<T>(lds_v1, ws, ws.sb, p, m_use, tile_of(j) * BN);
         else
-            last_step<T>(lds_v0, ws, ws.sa, p, m_use);
+            last_step<T>(lds_v0, ws, ws.sa, p, m_use, tile_of(j) * BN);
     }
 
     // Epilogue. Softmax: O = O^T / l, LSE = (m + log2 l) ln 2 (+ the relative
