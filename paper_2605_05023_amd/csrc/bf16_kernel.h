@@ -302,12 +302,29 @@ __device__ __forceinline__ bool visible(const MaskThr& m, int c)
         return c <= m.hi;
 }
 
+// Per-tile bases of the position terms of this lane's row: with j the key
+// at element offset 0 of the lane (jn + 8 lh), i' - j and jref - j as floats;
+// an element at offset c then takes base - c.
+struct PosBase {
+    float abs, lin;
+};
+
+template <class T>
+__device__ __forceinline__ PosBase pos_base(const WaveState<T>& ws, int jn)
+{
+    if constexpr (T::BIAS == kBiasNone) return {0.0f, 0.0f};
+    const int j = jn + 8 * ws.lh;
+    return {(float)(ws.ip - j), (float)(ws.jref - j)};
+}
+
+// Final score of element offset c (units; see score_tile_u).
 template <class T>
 __device__ __forceinline__ float final_score(float x, const AttnParams& p, const WaveState<T>& ws,
-                                             int j)
+                                             const PosBase& pb, int c)
 {
-    return score_u<T::SOFTCAP, T::BIAS>(x, p.scale_u, p.softcap_pre, p.softcap_post_u,
-                                         ws.bias_abs, ws.bias_lin, ws.ip, ws.jref, j);
+    return score_tile_u<T::SOFTCAP, T::BIAS>(x, p.scale_u, p.softcap_pre, p.softcap_post_u,
+                                              ws.bias_abs, ws.bias_lin, pb.abs - (float)c,
+                                              pb.lin - (float)c);
 }
 
 // S^T = K Q^T for the K tile in LDS at `kt`.
@@ -332,15 +349,15 @@ __device__ __forceinline__ float mods_and_max(f32x16 (&s)[T::NB], const AttnPara
 {
     float mx = -__builtin_inff();
     const MaskThr mt = mask_thresholds(ws, j0);
+    const PosBase pb = pos_base(ws, j0);
 #pragma unroll
     for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
             // element (b, e) is key j0 + 8lh + c, c = 32b + e + (e >= 8 ? 8 : 0)
             const int c = 32 * b + e + (e >= 8 ? 8 : 0);
-            const int j = j0 + 8 * ws.lh + c;
             float x = s[b][e];
-            if constexpr (T::MODS) x = final_score<T>(x, p, ws, j);
+            if constexpr (T::MODS) x = final_score<T>(x, p, ws, pb, c);
             if constexpr (MASKED)
                 if (!visible<T>(mt, c)) x = -__builtin_inff();
             s[b][e] = x;
@@ -568,6 +585,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     });
     check_tile<T>(ws, sc, pw, rs, p, jc);
     const MaskThr mt = mask_thresholds(ws, jn);
+    const PosBase pb = pos_base(ws, jn);
     static_for<PV>([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = ic.value;
         constexpr int b = i / (2 * DBLK), u = (i / DBLK) % 2, d = i % DBLK;
@@ -582,7 +600,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             // element (bb, e) is key jn + 8lh + c, c = 32bb + e + (e >= 8 ? 8 : 0)
             constexpr int c = 32 * bb + e + (e >= 8 ? 8 : 0);
             float x = sn[bb][e];
-            if constexpr (T::MODS) x = final_score<T>(x, p, ws, jn + 8 * ws.lh + c);
+            if constexpr (T::MODS) x = final_score<T>(x, p, ws, pb, c);
             if constexpr (MASKED)
                 if (!visible<T>(mt, c)) x = -__builtin_inff();
             sn[bb][e] = x;

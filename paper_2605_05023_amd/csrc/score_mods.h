@@ -65,6 +65,39 @@ __device__ __forceinline__ float score_u(float dot, float scale_u, float softcap
     return t;
 }
 
+// C' tanh(dot * pre) with C' = C * unit, the soft-cap of score_u with the
+// outer product folded into the last step of each branch: for |y| < 1/16,
+// C' y (1 - y^2 / 3); elsewhere C' - 2 C' / (1 + e^(2y)) (same accuracy as
+// tanh_f32).
+__device__ __forceinline__ float softcap_u(float dot, float pre, float cu)
+{
+    const float y = dot * pre;
+    const float small = y * __builtin_fmaf(y * y, cu * (-1.0f / 3.0f), cu);
+    const float e = __builtin_amdgcn_exp2f(y * (2.0f * kLog2e));
+    const float big = __builtin_fmaf(-2.0f * cu, __builtin_amdgcn_rcpf(1.0f + e), cu);
+    return __builtin_fabsf(y) < 0.0625f ? small : big;
+}
+
+// score_u for the bf16 kernels, with the position terms taken as floats:
+// dabs = i' - j and dlin = jref - j, which the kernels form as a per-tile
+// base minus the key's compile-time offset within the tile.
+template <bool SOFTCAP, int BIAS>
+__device__ __forceinline__ float score_tile_u(float dot, float scale_u, float softcap_pre,
+                                              float softcap_post_u, float bias_abs, float bias_lin,
+                                              float dabs, float dlin)
+{
+    float t;
+    if constexpr (SOFTCAP)
+        t = softcap_u(dot, softcap_pre, softcap_post_u);
+    else
+        t = dot * scale_u;
+    if constexpr (BIAS == kBiasAlibi || BIAS == kBiasGeneral)
+        t = __builtin_fmaf(bias_abs, __builtin_fabsf(dabs), t);
+    if constexpr (BIAS == kBiasRelPos || BIAS == kBiasGeneral)
+        t = __builtin_fmaf(bias_lin, dlin, t);
+    return t;
+}
+
 // ReLU(x) and Sigmoid(x) of a natural score; a masked score (-inf) maps to 0.
 template <int NORM>
 __device__ __forceinline__ float activation(float x)
