@@ -162,6 +162,67 @@ def test_unequal_lengths(sq, sk, mask, wl, wr, dtype):
         assert (og[:, :, : sq - sk] == 0).all()
 
 
+# Packed batches whose sequences have different query and key lengths: one
+# query against a cache (decode), a query chunk against a longer key history
+# (chunked prefill), more queries than keys (rows with no visible key under
+# the bottom-right aligned causal mask) and empty query or key sides.
+VARLEN_QK = [
+    ("bf16_d128_decode_causal_gqa", "bf16", 8, 2, 128, dict(causal=True),
+     [(1, 300), (1, 1), (1, 64), (1, 0), (1, 129)]),
+    ("bf16_d128_chunked_prefill_window", "bf16", 4, 1, 128, dict(window=(100, 0)),
+     [(64, 320), (130, 130), (0, 50), (17, 200)]),
+    ("bf16_d64_more_queries_causal", "bf16", 4, 4, 64, dict(causal=True),
+     [(200, 70), (5, 0), (129, 128)]),
+    ("bf16_d64_alibi_softcap_none", "bf16", 4, 2, 64, dict(alibi=True, softcap=30.0),
+     [(33, 257), (129, 1), (70, 0)]),
+    ("fp32_d128_chunked_prefill_causal", "fp32", 4, 2, 128, dict(causal=True),
+     [(65, 200), (1, 30), (100, 90)]),
+]
+
+
+@pytest.mark.parametrize("case", VARLEN_QK, ids=[c[0] for c in VARLEN_QK])
+def test_varlen_unequal_lengths(case):
+    name, dtype, hq, hkv, D, variant, lens = case
+    log(f"[parity varlen q!=k] {name} (lq, lk) = {lens}")
+    g = torch.Generator().manual_seed(9)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    lq = [a for a, _ in lens]
+    lk = [b for _, b in lens]
+    cuq = torch.tensor([0] + list(np.cumsum(lq)), dtype=torch.int32)
+    cuk = torch.tensor([0] + list(np.cumsum(lk)), dtype=torch.int32)
+    q = torch.randn((sum(lq), hq, D), generator=g).to(tdt)
+    k = (1.5 * torch.randn((sum(lk), hkv, D), generator=g)).to(tdt)
+    v = torch.randn((sum(lk), hkv, D), generator=g).to(tdt)
+    slopes = None
+    if variant.get("alibi"):
+        slopes = torch.tensor([2.0 ** (-8.0 * (h + 1) / hq) for h in range(hq)],
+                              dtype=torch.float32)
+    softcap = variant.get("softcap", 0.0)
+    wl, wr = variant.get("window", (-1, -1))
+    mask = WINDOW if "window" in variant else CAUSAL if variant.get("causal") else NONE
+    dev = "cuda:0"
+    o, lse = fwd(q.to(dev), k.to(dev), v.to(dev), causal=variant.get("causal", False),
+                 window=variant.get("window"), softcap=softcap,
+                 alibi_slopes=slopes.to(dev) if slopes is not None else None,
+                 cu_seqlens_q=cuq.to(dev), cu_seqlens_k=cuk.to(dev),
+                 max_seqlen_q=max(lq), max_seqlen_k=max(lk))
+    torch.cuda.synchronize()
+    o_ref, lse_ref = oracle.attention(q, k, v, scale=D ** -0.5, mask=mask, window_left=wl,
+                                      window_right=wr, slopes=slopes, softcap=softcap,
+                                      cu_seqlens_q=cuq, cu_seqlens_k=cuk)
+    og = o.float().cpu().numpy()
+    lg = lse.cpu().numpy().astype(np.float64)
+    o_err = float(np.abs(og - o_ref).max()) if og.size else 0.0
+    log(f"  {name}: max|dO| = {o_err:.3e}")
+    assert o_err <= (2e-2 if dtype == "bf16" else 1e-4)
+    assert np.array_equal(np.isinf(lg), np.isinf(lse_ref)), "LSE -inf pattern differs"
+    fin = np.isfinite(lse_ref)
+    if fin.any():
+        assert np.abs(lg[fin] - lse_ref[fin]).max() <= 1e-3
+    # rows that see no key (empty key side, or causal rows above the diagonal)
+    assert (og[np.isinf(lse_ref).T] == 0).all()
+
+
 @pytest.mark.parametrize("name", WORKLOAD_ORDER)
 def test_workload_full_size(name):
     """Each workload at full size, in the benchmark's launch configuration."""
