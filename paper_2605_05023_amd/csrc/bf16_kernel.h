@@ -123,6 +123,14 @@ __device__ __forceinline__ int chunk_swizzle(int key)
         return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
 }
 
+// s_waitcnt immediate that waits until at most n vector memory operations are
+// outstanding and leaves the other counters unconstrained (gfx9 encoding:
+// vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+__device__ constexpr int vmcnt_only(int n)
+{
+    return (n & 0xF) | (0x7 << 4) | (0xF << 8) | ((n >> 4) << 14);
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes)
 {
     // dword3 0x00020000: 32-bit untyped data format, no swizzle (gfx9 family)
@@ -340,6 +348,17 @@ __device__ __forceinline__ void qk_tile(const char* kt, const WaveState<T>& ws, 
                                                            0, 0);
         }
     }
+    // Issue order: K reads AHEAD products ahead, then one product and one read
+    // at a time, so each accumulation chain runs back to back (a product that
+    // depends on the one two before it would stall).
+    constexpr int N = T::NB * T::KSTEPS, AHEAD = 4;
+    __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);  // DS read
+#pragma unroll
+    for (int i = 0; i < N - AHEAD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, AHEAD, 0);
 }
 
 // Score mods, element mask (MASKED) and the tile's row max, in log2 units.
@@ -861,9 +880,13 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         const int t0 = tile_of(jbeg);
         issue_tile<T>(lds_k0, krs, t0 * BN, krow, klp, wave);
         issue_tile<T>(lds_v0, vrs, t0 * BN, vrow, vlp, wave);
-        if (jbeg + 1 < jend) issue_tile<T>(lds_k1, krs, tile_of(jbeg + 1) * BN, krow, klp, wave);
-        __builtin_amdgcn_s_waitcnt(0);  // this thread's loads have landed in LDS
-        __syncthreads();
+        // past the last tile K_lo+1 reads rows beyond the sequence end (zeros)
+        issue_tile<T>(lds_k1, krs, jbeg + 1 < jend ? tile_of(jbeg + 1) * BN : lk, krow, klp, wave);
+        // Q and K_lo have landed (V_lo and K_lo+1, the last 2 LOADS direct
+        // loads, may still be in flight: the barrier after the first tile's
+        // max waits for them)
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(2 * T::LOADS));
+        asm volatile("s_barrier" ::: "memory");  // no LDS access moves across it
         qk_tile<T>(lds_k0, ws, ws.sa);
         bool masked_lo;
         if constexpr (T::GEN)
