@@ -281,6 +281,23 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
         if (c >= 1 && c <= groups_per_xcd) p.chunk = c;
     }
+    // Divisors of the workgroup-id decode (all >= 1; blocks <= INT32_MAX
+    // bounds every dividend).
+    p.div_bh = make_fastdiv((uint32_t)(d.batch * d.num_q_heads));
+    p.div_hq = make_fastdiv((uint32_t)d.num_q_heads);
+    p.div_group = make_fastdiv((uint32_t)p.group);
+    p.div_hkv = make_fastdiv((uint32_t)d.num_kv_heads);
+    p.div_chunk_items = p.div_chunk_full = p.div_chunk_last = make_fastdiv(1);
+    p.last_chunk = 0;
+    if (p.map_mode == 1) {
+        const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
+        const int64_t last = (groups_per_xcd + p.chunk - 1) / p.chunk - 1;
+        const int64_t last_groups = groups_per_xcd - last * p.chunk;
+        p.div_chunk_items = make_fastdiv((uint32_t)((int64_t)p.chunk * p.group * q_tiles));
+        p.div_chunk_full = make_fastdiv((uint32_t)(p.chunk * p.group));
+        p.div_chunk_last = make_fastdiv((uint32_t)(last_groups * p.group));
+        p.last_chunk = (int32_t)last;
+    }
     hipStream_t stream = static_cast<hipStream_t>(d.stream);
     hipError_t err = d.dtype == ATTN_BF16 ? attn::launch_bf16(p, d.head_dim, stream)
                                           : attn::launch_f32(p, d.head_dim, stream);

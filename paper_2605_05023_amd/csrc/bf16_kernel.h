@@ -205,7 +205,7 @@ __device__ __forceinline__ float pair_sum(float x)
 }
 
 struct WorkItem {
-    int b, hq, qt;
+    int b, hq, hkv, qt;
 };
 
 // Compile-time loop: f(std::integral_constant<int, i>) for i = 0..N-1, so
@@ -244,27 +244,34 @@ struct Bool {
 // tiles are shared through that XCD's L2.
 __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
 {
+    // every divisor is launch-invariant: multiply-high and shift (fastdiv.h)
     WorkItem it;
-    int nbh = p.batch * p.hq;
+    const uint32_t uw = (uint32_t)w;
+    int qt_rev;
     if (p.map_mode == 1) {
-        int x = w & 7, k = w >> 3;
-        int groups_per_xcd = (p.batch * p.hkv) >> 3;
-        int chunk_items = p.chunk * p.group * p.num_q_tiles;
-        int c = k / chunk_items;
-        int cg = min(p.chunk, groups_per_xcd - c * p.chunk);  // groups in this chunk
-        int rem = k - c * chunk_items;
-        int qt_rev = rem / (cg * p.group), r2 = rem % (cg * p.group);
-        int gi = c * p.chunk + r2 / p.group, r = r2 % p.group;
-        int g = x + 8 * gi;
-        it.b = g / p.hkv;
-        it.hq = (g % p.hkv) * p.group + r;
-        it.qt = p.q_order ? qt_rev : p.num_q_tiles - 1 - qt_rev;
+        const uint32_t x = uw & 7, k = uw >> 3;
+        const uint32_t c = fast_div(k, p.div_chunk_items);
+        const uint32_t rem = k - c * p.div_chunk_items.d;
+        // (query head in group, group in chunk) pairs of this chunk
+        const FastDiv pairs = (int)c == p.last_chunk ? p.div_chunk_last : p.div_chunk_full;
+        qt_rev = (int)fast_div(rem, pairs);
+        const uint32_t r2 = rem - (uint32_t)qt_rev * pairs.d;
+        const uint32_t gq = fast_div(r2, p.div_group);
+        const int r = (int)(r2 - gq * p.div_group.d);
+        const uint32_t g = x + 8 * (c * (uint32_t)p.chunk + gq);
+        const uint32_t b = fast_div(g, p.div_hkv);
+        it.b = (int)b;
+        it.hkv = (int)(g - b * p.div_hkv.d);
+        it.hq = it.hkv * p.group + r;
     } else {
-        int qt_rev = w / nbh, rem = w % nbh;
-        it.b = rem / p.hq;
-        it.hq = rem % p.hq;
-        it.qt = p.q_order ? qt_rev : p.num_q_tiles - 1 - qt_rev;
+        qt_rev = (int)fast_div(uw, p.div_bh);
+        const uint32_t rem = uw - (uint32_t)qt_rev * p.div_bh.d;
+        const uint32_t b = fast_div(rem, p.div_hq);
+        it.b = (int)b;
+        it.hq = (int)(rem - b * p.div_hq.d);
+        it.hkv = (int)fast_div((uint32_t)it.hq, p.div_group);
     }
+    it.qt = p.q_order ? qt_rev : p.num_q_tiles - 1 - qt_rev;
     return it;
 }
 
@@ -750,7 +757,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     }
     const int q0 = it.qt * BM;
     if (q0 >= lq) return;  // whole workgroup: tile past this sequence's end
-    const int hkv = it.hq / p.group;
+    const int hkv = it.hkv;
 
     const __bf16* qb = static_cast<const __bf16*>(p.q);
     const __bf16* kbase = static_cast<const __bf16*>(p.k);

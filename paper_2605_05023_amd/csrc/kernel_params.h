@@ -4,6 +4,7 @@
 
 #include <stdint.h>
 
+#include "fastdiv.h"
 #include "plan.h"
 
 struct AttnParams {
@@ -22,6 +23,15 @@ struct AttnParams {
     int32_t map_mode;        // workgroup order (0 natural, 1 kv-group per XCD)
     int32_t q_order;         // query tiles issued 0 last-first (causal-like), 1 first-first
     int32_t chunk;           // map_mode 1: kv-head groups per chunk within an XCD
+    // The divisors of the workgroup-id decode, prepared for fast_div.
+    FastDiv div_bh;          // batch * hq                    (map_mode 0)
+    FastDiv div_hq;          // hq                            (map_mode 0)
+    FastDiv div_chunk_items; // chunk * group * num_q_tiles   (map_mode 1)
+    FastDiv div_chunk_full;  // chunk * group: a full chunk's (head, group) pairs
+    FastDiv div_chunk_last;  // the same for the last chunk of an XCD
+    FastDiv div_group;       // group
+    FastDiv div_hkv;         // hkv
+    int32_t last_chunk;      // index of an XCD's last chunk
     int64_t total_q;         // varlen: rows of the [Hq, total_q] LSE
     // element strides
     int64_t sq_b, sq_h, sq_s;
