@@ -646,6 +646,9 @@ template <class T>
 __device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, f32x16 (&sc)[T::NB],
                                           const AttnParams& p, float m_use, int jc)
 {
+    // No row of this wave sees the tile (the diagonal tile of the upper rows
+    // under causal-like masks): P is zero, nothing to add.
+    if (!__builtin_amdgcn_ballot_w64(row_sees_tile(ws, jc))) return;
     u32x4 pw[T::NB][2];
     const float rs = exp_tile<T>(sc, pw, m_use, p.scale_u);
     check_tile<T>(ws, sc, pw, rs, p, jc);
