@@ -53,6 +53,10 @@ SMALL = [
     W("bf16_d128_alibi_causal", "bf16", 1, 4, 4, 200, 128, CAUSAL, alibi=True),
     W("bf16_d64_softcap_causal", "bf16", 1, 2, 2, 190, 64, CAUSAL, softcap=30.0),
     W("bf16_d64_softcap_1e4", "bf16", 1, 2, 2, 150, 64, softcap=1e4),
+    W("bf16_d128_softcap_causal", "bf16", 1, 4, 2, 300, 128, CAUSAL, softcap=30.0),
+    W("bf16_d128_softcap_window", "bf16", 1, 2, 2, 333, 128, WINDOW, 70, 0, softcap=30.0),
+    dataclasses.replace(W("bf16_d128_relpos_softcap", "bf16", 2, 2, 2, 200, 128, CAUSAL,
+                          softcap=20.0), relpos=True),
     W("fp32_d64_plain", "fp32", 1, 2, 2, 128, 64),
     W("fp32_d128_causal_gqa", "fp32", 2, 4, 2, 150, 128, CAUSAL),
     W("fp32_d64_window", "fp32", 1, 2, 2, 200, 64, WINDOW, 20, 3),
@@ -92,6 +96,7 @@ RAMPS = [
     ("bf16_d128_window_up", "bf16", 128, WINDOW, 100, 0, 0.0, 150.0),
     ("bf16_d64_causal_up", "bf16", 64, CAUSAL, -1, -1, 0.0, 150.0),
     ("bf16_d64_softcap_up", "bf16", 64, NONE, -1, -1, 1e4, 150.0),
+    ("bf16_d128_softcap_up", "bf16", 128, CAUSAL, -1, -1, 1e4, 150.0),
     ("fp32_d64_causal_up", "fp32", 64, CAUSAL, -1, -1, 0.0, 150.0),
 ]
 
