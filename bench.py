@@ -235,30 +235,26 @@ def main():
     wall = time.perf_counter() - t0
     kernel_ms = e0.elapsed_time(e1) / args.steps
 
-    # Per-launch durations (HIP events around each call on the same stream),
-    # outside the timed region: median and minimum, with the caches warm and
-    # after a 512 MiB write that evicts the inputs from the L2s and the 256 MB
-    # Infinity Cache.
-    reps = max(1, min(args.steps, 50))
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(reps)]
-    for a, b in ev:
-        a.record(stream)
-        step()
-        b.record(stream)
-    torch.cuda.synchronize()
-    warm = sorted(a.elapsed_time(b) for a, b in ev)
+    # Per-launch durations, outside the timed region, from HIP events queued
+    # around each launch on the same stream (no host wait in between): launches
+    # with warm caches alternate with launches after a 512 MiB write that
+    # evicts the inputs from the L2s and the 256 MB Infinity Cache, so that the
+    # drift of the power-limited clock under sustained load affects both alike.
+    reps = max(1, min(args.steps, 30))
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    cold = []
-    for a, b in ev[: min(reps, 20)]:
-        flush.fill_(0)
-        a.record(stream)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+    for w0, w1, c0, c1 in ev:
+        w0.record(stream)
         step()
-        b.record(stream)
-        torch.cuda.synchronize()
-        cold.append(a.elapsed_time(b))
+        w1.record(stream)
+        flush.fill_(0)
+        c0.record(stream)
+        step()
+        c1.record(stream)
+    torch.cuda.synchronize()
+    warm = sorted(w0.elapsed_time(w1) for w0, w1, _, _ in ev)
+    cold = sorted(c0.elapsed_time(c1) for _, _, c0, c1 in ev)
     del flush
-    cold.sort()
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
