@@ -209,9 +209,21 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         !slice_fits(max_k, p.sv_s, D, elt, 128) || !slice_fits(max_q, p.so_s, D, elt, 128))
         return ATTN_ERR_UNSUPPORTED;
 
-    const int block_m = d.dtype == ATTN_BF16 ? attn::bf16_block_m() : attn::f32_block_m();
-    const int64_t q_tiles = (max_q + block_m - 1) / block_m;
-    const int64_t blocks = q_tiles * d.num_q_heads * (int64_t)d.batch;
+    // bf16: the query heads of one kv group share a workgroup, up to four of
+    // them (one 32-row block each), so every K/V tile in LDS serves all of
+    // them and the workgroup's 128 (head, row) pairs span only 32 positions,
+    // which leaves fewer partially visible tiles at the mask edges.
+    const int group = d.num_q_heads / d.num_kv_heads;
+    int hp = d.dtype != ATTN_BF16 ? 1 : group % 4 == 0 ? 4 : group % 2 == 0 ? 2 : 1;
+    if (const char* env = std::getenv("ATTN_HEADS_PER_WG")) {  // experiments: 1, 2 or 4
+        const int h = std::atoi(env);
+        if (d.dtype == ATTN_BF16 && (h == 1 || h == 2 || h == 4) && group % h == 0) hp = h;
+    }
+    const int block_m = d.dtype == ATTN_BF16 ? attn::bf16_block_m() / hp : attn::f32_block_m();
+    // a multiple of hp: the hp query tiles of one 128-row span are issued
+    // together (their K/V reads then meet in the L2)
+    const int64_t q_tiles = (max_q + hp * block_m - 1) / (hp * block_m) * hp;
+    const int64_t blocks = q_tiles * (d.num_q_heads / hp) * (int64_t)d.batch;
     if (blocks > INT32_MAX) return ATTN_ERR_UNSUPPORTED;
     if (blocks == 0) return ATTN_OK;  // nothing to compute
 
@@ -232,7 +244,10 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.batch = d.batch;
     p.hq = d.num_q_heads;
     p.hkv = d.num_kv_heads;
-    p.group = d.num_q_heads / d.num_kv_heads;
+    p.group = group;
+    p.hp = hp;
+    p.hp_shift = hp == 4 ? 2 : hp == 2 ? 1 : 0;
+    p.wg_rows = block_m;
     p.seqlen_q = d.seqlen_q;
     p.seqlen_k = d.seqlen_k;
     p.num_q_tiles = (int32_t)q_tiles;
@@ -266,7 +281,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
         const int64_t kv_tokens = varlen ? d.total_k : (int64_t)d.batch * d.seqlen_k;
         const int64_t kv_bytes = kv_tokens * d.num_kv_heads * D * elt * 2;
-        const int64_t per_group = (int64_t)p.group * q_tiles;
+        const int64_t per_group = (int64_t)(p.group / hp) * q_tiles;  // workgroups of a kv group
         int64_t chunk = groups_per_xcd;
         if (kv_bytes > (int64_t)320 << 20) chunk = (64 + per_group - 1) / per_group;
         if (chunk > groups_per_xcd) chunk = groups_per_xcd;
@@ -283,9 +298,10 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     }
     // Divisors of the workgroup-id decode (all >= 1; blocks <= INT32_MAX
     // bounds every dividend).
-    p.div_bh = make_fastdiv((uint32_t)(d.batch * d.num_q_heads));
-    p.div_hq = make_fastdiv((uint32_t)d.num_q_heads);
-    p.div_group = make_fastdiv((uint32_t)p.group);
+    const int hsets = d.num_q_heads / hp, gsets = group / hp;
+    p.div_bh = make_fastdiv((uint32_t)(d.batch * hsets));
+    p.div_hq = make_fastdiv((uint32_t)hsets);
+    p.div_group = make_fastdiv((uint32_t)gsets);
     p.div_hkv = make_fastdiv((uint32_t)d.num_kv_heads);
     p.div_chunk_items = p.div_chunk_full = p.div_chunk_last = make_fastdiv(1);
     p.last_chunk = 0;
@@ -293,9 +309,9 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
         const int64_t last = (groups_per_xcd + p.chunk - 1) / p.chunk - 1;
         const int64_t last_groups = groups_per_xcd - last * p.chunk;
-        p.div_chunk_items = make_fastdiv((uint32_t)((int64_t)p.chunk * p.group * q_tiles));
-        p.div_chunk_full = make_fastdiv((uint32_t)(p.chunk * p.group));
-        p.div_chunk_last = make_fastdiv((uint32_t)(last_groups * p.group));
+        p.div_chunk_items = make_fastdiv((uint32_t)((int64_t)p.chunk * gsets * q_tiles));
+        p.div_chunk_full = make_fastdiv((uint32_t)(p.chunk * gsets));
+        p.div_chunk_last = make_fastdiv((uint32_t)(last_groups * gsets));
         p.last_chunk = (int32_t)last;
     }
     hipStream_t stream = static_cast<hipStream_t>(d.stream);

@@ -1,8 +1,11 @@
 // bf16_kernel.h -- fused attention forward for bf16 inputs on gfx950 (kernel
 // template; instantiated by the attn_fwd_bf16*.hip translation units).
 //
-// One workgroup computes BM = 128 query rows of one (sequence, query head):
-// four wavefronts of 32 rows each. It streams the key/value tiles of BN keys
+// One workgroup computes BM = 128 (query head, query row) pairs of one
+// sequence: four wavefronts of 32 rows each, either 128 rows of one head or,
+// when query heads share a kv head (grouped-query attention), the same 32 or
+// 64 rows of the four or two heads of one kv group, which then share every
+// K/V tile in LDS. It streams the key/value tiles of BN keys
 // (32 or 64) that the mask leaves visible through LDS, computes the scores on the
 // bf16 matrix cores with fp32 accumulation, applies the score modifications
 // and, on partial tiles only, the mask in registers, keeps an online softmax
@@ -67,7 +70,7 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int BM = 128;      // query rows per workgroup
+constexpr int BM = 128;      // (query head, query row) pairs per workgroup
 constexpr int NT = 256;      // threads per workgroup (4 waves)
 // Softmax with score mods keeps a lazily updated running max: it moves only
 // when a tile's max exceeds it by more than TAU (log2 units), so P <= 2^TAU.
@@ -204,6 +207,7 @@ __device__ __forceinline__ float pair_sum(float x)
     return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
 }
 
+// Sequence, first query head of the workgroup's head set, kv head, query tile.
 struct WorkItem {
     int b, hq, hkv, qt;
 };
@@ -232,10 +236,13 @@ struct Bool {
     static constexpr bool value = V;
 };
 
-// Map the hardware workgroup id to (sequence, query head, query tile).
+// Map the hardware workgroup id to (sequence, query head set, query tile).
 // Query tiles are issued longest-first: the last tiles of a causal sequence
 // see the most keys, so the order is descending unless the host asks for
 // ascending (q_order = 1: the first tiles are the heaviest, e.g. global rows).
+// With hp heads per workgroup (32 * 4 / hp rows), the hp query tiles of one
+// 128-row span of a head set have consecutive ids, so they start together
+// on one XCD and read the same K/V tiles at about the same time.
 // Within an XCD the kv-head groups are taken `chunk` at a time (every query
 // head and query tile of the chunk, longest-first inside it), so the K/V
 // tiles in use at any moment belong to a few groups and stay in that XCD's
@@ -252,24 +259,29 @@ __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
         const uint32_t x = uw & 7, k = uw >> 3;
         const uint32_t c = fast_div(k, p.div_chunk_items);
         const uint32_t rem = k - c * p.div_chunk_items.d;
-        // (query head in group, group in chunk) pairs of this chunk
+        const uint32_t lo = rem & (uint32_t)(p.hp - 1), rest = rem >> p.hp_shift;
+        // (head set in group, group in chunk) pairs of this chunk
         const FastDiv pairs = (int)c == p.last_chunk ? p.div_chunk_last : p.div_chunk_full;
-        qt_rev = (int)fast_div(rem, pairs);
-        const uint32_t r2 = rem - (uint32_t)qt_rev * pairs.d;
+        const uint32_t hi = fast_div(rest, pairs);
+        qt_rev = (int)((hi << p.hp_shift) + lo);
+        const uint32_t r2 = rest - hi * pairs.d;
         const uint32_t gq = fast_div(r2, p.div_group);
-        const int r = (int)(r2 - gq * p.div_group.d);
+        const int r = (int)(r2 - gq * p.div_group.d);  // head set within the group
         const uint32_t g = x + 8 * (c * (uint32_t)p.chunk + gq);
         const uint32_t b = fast_div(g, p.div_hkv);
         it.b = (int)b;
         it.hkv = (int)(g - b * p.div_hkv.d);
-        it.hq = it.hkv * p.group + r;
+        it.hq = it.hkv * p.group + (r << p.hp_shift);
     } else {
-        qt_rev = (int)fast_div(uw, p.div_bh);
-        const uint32_t rem = uw - (uint32_t)qt_rev * p.div_bh.d;
+        const uint32_t lo = uw & (uint32_t)(p.hp - 1), rest = uw >> p.hp_shift;
+        const uint32_t hi = fast_div(rest, p.div_bh);
+        qt_rev = (int)((hi << p.hp_shift) + lo);
+        const uint32_t rem = rest - hi * p.div_bh.d;
         const uint32_t b = fast_div(rem, p.div_hq);
+        const uint32_t hs = rem - b * p.div_hq.d;  // head set
         it.b = (int)b;
-        it.hq = (int)(rem - b * p.div_hq.d);
-        it.hkv = (int)fast_div((uint32_t)it.hq, p.div_group);
+        it.hq = (int)(hs << p.hp_shift);
+        it.hkv = (int)fast_div(hs, p.div_group);
     }
     it.qt = p.q_order ? qt_rev : p.num_q_tiles - 1 - qt_rev;
     return it;
@@ -758,9 +770,14 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         lq = p.seqlen_q;
         lk = p.seqlen_k;
     }
-    const int q0 = it.qt * BM;
+    const int q0 = it.qt * p.wg_rows;
     if (q0 >= lq) return;  // whole workgroup: tile past this sequence's end
     const int hkv = it.hkv;
+    // Wave w takes query head hq + (w mod hp) and the 32-row block w / hp of
+    // the workgroup's rows (hp = 1: four row blocks of one head; hp = 4: the
+    // same 32 rows of four heads that share the K/V tiles).
+    const int hq = it.hq + (wave & (p.hp - 1));
+    const int rblk = wave >> p.hp_shift;
 
     const __bf16* qb = static_cast<const __bf16*>(p.q);
     const __bf16* kbase = static_cast<const __bf16*>(p.k);
@@ -768,13 +785,13 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     __bf16* ob = static_cast<__bf16*>(p.o);
     int64_t qoff, koff, voff, ooff;
     if (p.cu_q) {
-        qoff = qrow0 * p.sq_s + (int64_t)it.hq * p.sq_h;
-        ooff = qrow0 * p.so_s + (int64_t)it.hq * p.so_h;
+        qoff = qrow0 * p.sq_s + (int64_t)hq * p.sq_h;
+        ooff = qrow0 * p.so_s + (int64_t)hq * p.so_h;
         koff = krow0 * p.sk_s + (int64_t)hkv * p.sk_h;
         voff = krow0 * p.sv_s + (int64_t)hkv * p.sv_h;
     } else {
-        qoff = (int64_t)it.b * p.sq_b + (int64_t)it.hq * p.sq_h;
-        ooff = (int64_t)it.b * p.so_b + (int64_t)it.hq * p.so_h;
+        qoff = (int64_t)it.b * p.sq_b + (int64_t)hq * p.sq_h;
+        ooff = (int64_t)it.b * p.so_b + (int64_t)hq * p.so_h;
         koff = (int64_t)it.b * p.sk_b + (int64_t)hkv * p.sk_h;
         voff = (int64_t)it.b * p.sv_b + (int64_t)hkv * p.sv_h;
     }
@@ -783,8 +800,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
 
     WaveState<T> ws;
     ws.lh = lh;
-    // Q fragment: lane holds row q0 + 32*wave + li, dims 16t + 8lh .. +7.
-    const int qi = q0 + wave * 32 + li;
+    // Q fragment: lane holds row q0 + 32*rblk + li, dims 16t + 8lh .. +7.
+    const int qi = q0 + rblk * 32 + li;
     {
         uint32_t bytes = (uint32_t)((((int64_t)lq - 1) * p.sq_s + D) * 2);
         __amdgpu_buffer_rsrc_t qrs = make_rsrc(qb + qoff, bytes);
@@ -851,7 +868,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         jend = tr.n;
     } else {
         if (qi < lq) band_row(p.band, qi, lq, lk, &ws.jlo, &ws.jhi);
-        gp = plan_tiles(p.band, q0, BM, lq, lk, BN);
+        gp = plan_tiles(p.band, q0, p.wg_rows, lq, lk, BN);
         jbeg = gp.lo;
         jend = gp.hi;
     }
@@ -860,10 +877,10 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     ws.jref = T::SOFTMAX ? (ws.pfx > 0 ? 0 : ws.jlo) : ws.ip;
     ws.bias_abs = 0.0f;
     ws.bias_lin = 0.0f;
-    if constexpr (T::BIAS == kBiasAlibi) ws.bias_abs = -p.slopes[it.hq] * p.unit;
+    if constexpr (T::BIAS == kBiasAlibi) ws.bias_abs = -p.slopes[hq] * p.unit;
     if constexpr (T::BIAS == kBiasRelPos) ws.bias_lin = p.unit;
     if constexpr (T::BIAS == kBiasGeneral) {
-        if (p.slopes) ws.bias_abs = -p.slopes[it.hq] * p.unit;
+        if (p.slopes) ws.bias_abs = -p.slopes[hq] * p.unit;
         if (p.relpos) ws.bias_lin = p.unit;
     }
 
@@ -1025,8 +1042,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
                     lse = (ws.m_run + __builtin_log2f(l_tot)) * kLn2;
                     if (ws.bias_lin != 0.0f) lse += (float)(ws.ip - ws.jref);
                 }
-                int64_t idx = p.cu_q ? (int64_t)it.hq * p.total_q + qrow0 + qi
-                                     : ((int64_t)it.b * p.hq + it.hq) * lq + qi;
+                int64_t idx = p.cu_q ? (int64_t)hq * p.total_q + qrow0 + qi
+                                     : ((int64_t)it.b * p.hq + hq) * lq + qi;
                 p.lse[idx] = lse;
             }
         }
@@ -1049,7 +1066,7 @@ template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN, bool LEFT = true>
 hipError_t launch_variant(const AttnParams& p, hipStream_t stream)
 {
     using T = Traits<D, key_tile_width(D), SOFTCAP, BIAS, NORM, GEN, LEFT>;
-    int64_t blocks = (int64_t)p.num_q_tiles * p.hq * p.batch;
+    int64_t blocks = (int64_t)p.num_q_tiles * (p.hq >> p.hp_shift) * p.batch;
     hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)blocks), dim3(NT), 0, stream, p);
     return hipGetLastError();
 }

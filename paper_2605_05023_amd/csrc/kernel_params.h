@@ -18,18 +18,23 @@ struct AttnParams {
     const int32_t* cu_k;
     int32_t batch;           // B or number of sequences
     int32_t hq, hkv, group;  // group = hq / hkv
+    // bf16: query heads per workgroup (1, 2 or 4, heads of one kv group, one
+    // or two per wave row block) and query rows per workgroup (128 / hp)
+    int32_t hp, hp_shift, wg_rows;
     int32_t seqlen_q, seqlen_k;  // fixed length
     int32_t num_q_tiles;     // ceil(max query length / block_m)
     int32_t map_mode;        // workgroup order (0 natural, 1 kv-group per XCD)
     int32_t q_order;         // query tiles issued 0 last-first (causal-like), 1 first-first
     int32_t chunk;           // map_mode 1: kv-head groups per chunk within an XCD
     // The divisors of the workgroup-id decode, prepared for fast_div.
-    FastDiv div_bh;          // batch * hq                    (map_mode 0)
-    FastDiv div_hq;          // hq                            (map_mode 0)
-    FastDiv div_chunk_items; // chunk * group * num_q_tiles   (map_mode 1)
-    FastDiv div_chunk_full;  // chunk * group: a full chunk's (head, group) pairs
+    // A head set is the hp query heads of one workgroup; a kv group holds
+    // group / hp of them.
+    FastDiv div_bh;          // batch * hq / hp                    (map_mode 0)
+    FastDiv div_hq;          // hq / hp                            (map_mode 0)
+    FastDiv div_chunk_items; // chunk * group / hp * num_q_tiles   (map_mode 1)
+    FastDiv div_chunk_full;  // chunk * group / hp: a full chunk's (head set, group) pairs
     FastDiv div_chunk_last;  // the same for the last chunk of an XCD
-    FastDiv div_group;       // group
+    FastDiv div_group;       // group / hp
     FastDiv div_hkv;         // hkv
     int32_t last_chunk;      // index of an XCD's last chunk
     int64_t total_q;         // varlen: rows of the [Hq, total_q] LSE
