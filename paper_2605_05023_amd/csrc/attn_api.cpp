@@ -266,6 +266,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.scale_u = d.scale * p.unit;
     p.softcap = d.softcap;
     p.softcap_pre = d.softcap > 0.0f ? d.scale / d.softcap : 0.0f;
+    p.softcap_pre2 = p.softcap_pre * (float)(2.0 * 1.4426950408889634);
     p.softcap_post_u = d.softcap * p.unit;
     // Longest tiles first: the last query tiles under causal-like masks, the
     // first ones when global rows (which see every key) sit at the start.

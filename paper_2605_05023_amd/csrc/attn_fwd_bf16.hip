@@ -14,16 +14,13 @@ namespace {
 template <int D, bool LEFT>
 hipError_t launch_closed_form(const AttnParams& p, hipStream_t stream)
 {
-    const bool sc = p.softcap > 0.0f;
     const int bias = p.slopes ? kBiasAlibi : (p.relpos ? kBiasRelPos : kBiasNone);
-    if (sc) {
-        if (bias == kBiasAlibi) return launch_variant<D, true, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
-        if (bias == kBiasRelPos) return launch_variant<D, true, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
-        return launch_variant<D, true, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
-    }
-    if (bias == kBiasAlibi) return launch_variant<D, false, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
-    if (bias == kBiasRelPos) return launch_variant<D, false, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
-    return launch_variant<D, false, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
+    return with_cap(p, [&](auto cap) {
+        constexpr int C = decltype(cap)::value;
+        if (bias == kBiasAlibi) return launch_variant<D, C, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
+        if (bias == kBiasRelPos) return launch_variant<D, C, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
+        return launch_variant<D, C, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
+    });
 }
 
 }  // namespace

@@ -9,16 +9,13 @@ namespace {
 template <bool LEFT>
 hipError_t closed_form_d64(const AttnParams& p, hipStream_t stream)
 {
-    const bool sc = p.softcap > 0.0f;
     const int bias = p.slopes ? kBiasAlibi : (p.relpos ? kBiasRelPos : kBiasNone);
-    if (sc) {
-        if (bias == kBiasAlibi) return launch_variant<64, true, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
-        if (bias == kBiasRelPos) return launch_variant<64, true, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
-        return launch_variant<64, true, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
-    }
-    if (bias == kBiasAlibi) return launch_variant<64, false, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
-    if (bias == kBiasRelPos) return launch_variant<64, false, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
-    return launch_variant<64, false, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
+    return with_cap(p, [&](auto cap) {
+        constexpr int C = decltype(cap)::value;
+        if (bias == kBiasAlibi) return launch_variant<64, C, kBiasAlibi, kNormSoftmax, false, LEFT>(p, stream);
+        if (bias == kBiasRelPos) return launch_variant<64, C, kBiasRelPos, kNormSoftmax, false, LEFT>(p, stream);
+        return launch_variant<64, C, kBiasNone, kNormSoftmax, false, LEFT>(p, stream);
+    });
 }
 
 }  // namespace

@@ -84,15 +84,16 @@ constexpr float TAU = 8.0f;
 // from 1, where its bf16 rounding enters O unmatched by the fp32 row sum).
 constexpr float PSUM_BOUND = 256.0f;
 
-// D: head dim; BN: keys per tile; SOFTCAP: soft-cap on; BIAS: kBias*;
+// D: head dim; BN: keys per tile; CAP: kCap* (soft-cap form); BIAS: kBias*;
 // NORM: kNorm*; GEN: per-row visible ranges (general mask path); LEFT: the
 // band has a left bound (otherwise every row's first visible key is 0 and
 // partial tiles only check the right bound, which also masks keys past the
 // sequence end).
-template <int D_, int BN_, bool SOFTCAP_, int BIAS_, int NORM_, bool GEN_, bool LEFT_ = true>
+template <int D_, int BN_, int CAP_, int BIAS_, int NORM_, bool GEN_, bool LEFT_ = true>
 struct Traits {
     static constexpr int D = D_, BN = BN_;
-    static constexpr bool SOFTCAP = SOFTCAP_, MODS = SOFTCAP_ || BIAS_ != kBiasNone;
+    static constexpr int CAP = CAP_;
+    static constexpr bool SOFTCAP = CAP_ != kCapOff, MODS = SOFTCAP || BIAS_ != kBiasNone;
     static constexpr int BIAS = BIAS_, NORM = NORM_;
     static constexpr bool SOFTMAX = NORM_ == kNormSoftmax, GEN = GEN_, LEFT = LEFT_ || GEN_;
     // softmax without score mods whose rows all see the first visited tile
@@ -349,7 +350,9 @@ template <class T>
 __device__ __forceinline__ float final_score(float x, const AttnParams& p, const WaveState<T>& ws,
                                              const PosBase& pb, int c)
 {
-    return score_tile_u<T::SOFTCAP, T::BIAS>(x, p.scale_u, p.softcap_pre, p.softcap_post_u,
+    return score_tile_u<T::CAP, T::BIAS>(x, p.scale_u,
+                                         T::CAP == kCapShort ? p.softcap_pre2 : p.softcap_pre,
+                                         p.softcap_post_u,
                                               ws.bias_abs, ws.bias_lin, pb.abs - (float)c,
                                               pb.lin - (float)c);
 }
@@ -1062,13 +1065,23 @@ constexpr int key_tile_width(int)
 #endif
 }
 
-template <int D, bool SOFTCAP, int BIAS, int NORM, bool GEN, bool LEFT = true>
+template <int D, int CAP, int BIAS, int NORM, bool GEN, bool LEFT = true>
 hipError_t launch_variant(const AttnParams& p, hipStream_t stream)
 {
-    using T = Traits<D, key_tile_width(D), SOFTCAP, BIAS, NORM, GEN, LEFT>;
+    using T = Traits<D, key_tile_width(D), CAP, BIAS, NORM, GEN, LEFT>;
     int64_t blocks = (int64_t)p.num_q_tiles * (p.hq >> p.hp_shift) * p.batch;
     hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)blocks), dim3(NT), 0, stream, p);
     return hipGetLastError();
+}
+
+// Calls f(std::integral_constant<int, kCap*>) for the soft-cap form of the
+// launch: off, the short form up to C = kCapShortMax, the exact one above.
+template <class F>
+hipError_t with_cap(const AttnParams& p, F&& f)
+{
+    if (p.softcap <= 0.0f) return f(std::integral_constant<int, kCapOff>{});
+    if (p.softcap <= kCapShortMax) return f(std::integral_constant<int, kCapShort>{});
+    return f(std::integral_constant<int, kCapExact>{});
 }
 
 // The general-path instantiations of one normalisation: head dim, soft-cap,
@@ -1076,17 +1089,15 @@ hipError_t launch_variant(const AttnParams& p, hipStream_t stream)
 template <int NORM>
 hipError_t launch_general_norm(const AttnParams& p, int head_dim, hipStream_t stream)
 {
-    const bool sc = p.softcap > 0.0f, bias = p.slopes != nullptr || p.relpos != 0;
-    if (head_dim == 128) {
-        if (sc && bias) return launch_variant<128, true, kBiasGeneral, NORM, true>(p, stream);
-        if (sc) return launch_variant<128, true, kBiasNone, NORM, true>(p, stream);
-        if (bias) return launch_variant<128, false, kBiasGeneral, NORM, true>(p, stream);
-        return launch_variant<128, false, kBiasNone, NORM, true>(p, stream);
-    }
-    if (sc && bias) return launch_variant<64, true, kBiasGeneral, NORM, true>(p, stream);
-    if (sc) return launch_variant<64, true, kBiasNone, NORM, true>(p, stream);
-    if (bias) return launch_variant<64, false, kBiasGeneral, NORM, true>(p, stream);
-    return launch_variant<64, false, kBiasNone, NORM, true>(p, stream);
+    const bool bias = p.slopes != nullptr || p.relpos != 0;
+    return with_cap(p, [&](auto cap) {
+        constexpr int C = decltype(cap)::value;
+        if (head_dim == 128)
+            return bias ? launch_variant<128, C, kBiasGeneral, NORM, true>(p, stream)
+                        : launch_variant<128, C, kBiasNone, NORM, true>(p, stream);
+        return bias ? launch_variant<64, C, kBiasGeneral, NORM, true>(p, stream)
+                    : launch_variant<64, C, kBiasNone, NORM, true>(p, stream);
+    });
 }
 
 }  // namespace

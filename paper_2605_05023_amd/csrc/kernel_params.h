@@ -59,5 +59,6 @@ struct AttnParams {
     float scale_u;           // scale * unit
     float softcap;           // C, 0 = off
     float softcap_pre;       // scale / C
+    float softcap_pre2;      // 2 log2(e) scale / C
     float softcap_post_u;    // C * unit
 };

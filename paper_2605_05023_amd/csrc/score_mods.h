@@ -78,16 +78,40 @@ __device__ __forceinline__ float softcap_u(float dot, float pre, float cu)
     return __builtin_fabsf(y) < 0.0625f ? small : big;
 }
 
+// Soft-cap forms of the bf16 kernels, chosen per launch by C.
+enum : int {
+    kCapOff = 0,
+    kCapShort = 1,  // C <= kCapShortMax: C' - 2 C' / (1 + e^(2y)) alone
+    kCapExact = 2,  // softcap_u, both branches
+};
+// Near y = 0 the short form cancels: its absolute error stays about
+// 2.4e-7 C' (1 ulp of the reciprocal and of e^(2y) around 1/2 and 1), which
+// is at most 1e-4 in log2 units for C <= 256, below every tolerance of the
+// outputs (the ALiBi and relative-position terms, and the row max, are exact).
+// Larger C need the cubic branch.
+constexpr float kCapShortMax = 256.0f;
+
+// C' tanh(y) as C' - 2 C' / (1 + e^(2y)) with e^(2y) = 2^(dot * pre2),
+// pre2 = 2 log2(e) scale / C.
+__device__ __forceinline__ float softcap_short_u(float dot, float pre2, float cu)
+{
+    const float e = __builtin_amdgcn_exp2f(dot * pre2);
+    return __builtin_fmaf(-2.0f * cu, __builtin_amdgcn_rcpf(1.0f + e), cu);
+}
+
 // score_u for the bf16 kernels, with the position terms taken as floats:
 // dabs = i' - j and dlin = jref - j, which the kernels form as a per-tile
-// base minus the key's compile-time offset within the tile.
-template <bool SOFTCAP, int BIAS>
+// base minus the key's compile-time offset within the tile. `softcap_pre` is
+// scale / C for kCapExact and 2 log2(e) scale / C for kCapShort.
+template <int CAP, int BIAS>
 __device__ __forceinline__ float score_tile_u(float dot, float scale_u, float softcap_pre,
                                               float softcap_post_u, float bias_abs, float bias_lin,
                                               float dabs, float dlin)
 {
     float t;
-    if constexpr (SOFTCAP)
+    if constexpr (CAP == kCapShort)
+        t = softcap_short_u(dot, softcap_pre, softcap_post_u);
+    else if constexpr (CAP == kCapExact)
         t = softcap_u(dot, softcap_pre, softcap_post_u);
     else
         t = dot * scale_u;
