@@ -18,11 +18,13 @@ struct AttnParams {
     const int32_t* cu_k;
     int32_t batch;           // B or number of sequences
     int32_t hq, hkv, group;  // group = hq / hkv
-    // bf16: query heads per workgroup (1, 2 or 4, heads of one kv group, one
-    // or two per wave row block) and query rows per workgroup (128 / hp)
+    // bf16: query heads per workgroup hp (1, 2 or 4, all of one kv group;
+    // wave w takes head w mod hp), log2(hp), and query rows per workgroup
+    // (128 / hp; fp32: 64)
     int32_t hp, hp_shift, wg_rows;
     int32_t seqlen_q, seqlen_k;  // fixed length
-    int32_t num_q_tiles;     // ceil(max query length / block_m)
+    int32_t num_q_tiles;     // query tiles of wg_rows rows: ceil(max query length / 128) * hp
+                             // (bf16), ceil(max query length / 64) (fp32)
     int32_t map_mode;        // workgroup order (0 natural, 1 kv-group per XCD)
     int32_t q_order;         // query tiles issued 0 last-first (causal-like), 1 first-first
     int32_t chunk;           // map_mode 1: kv-head groups per chunk within an XCD

@@ -9,6 +9,7 @@ namespace attn {
 
 // bf16 inputs, fp32 accumulation; head_dim 64 or 128.
 hipError_t launch_bf16(const AttnParams& p, int head_dim, hipStream_t stream);
+// (query head, query row) pairs per workgroup of the bf16 kernel
 int bf16_block_m();
 // instantiation groups of the bf16 kernel, one translation unit each
 hipError_t launch_bf16_closed_form_d128(const AttnParams& p, hipStream_t stream);
