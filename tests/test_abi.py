@@ -110,6 +110,12 @@ CASES = [
     ("negative stride", lambda d: setattr(d, "stride_o_h", -128), "ATTN_ERR_BAD_SHAPE"),
     ("slice beyond 2 GiB", lambda d: (setattr(d, "seqlen_k", 1 << 20), setattr(d, "stride_k_s", 1 << 12)),
      "ATTN_ERR_UNSUPPORTED"),
+    # one key row past the largest slice the 32-bit offsets allow (with one
+    # tile of padding): ((Sk + 128) * 128 + 128) * 2 bytes reaches 2^31
+    ("slice one row past 2 GiB", lambda d: (setattr(d, "batch", 1), setattr(d, "num_q_heads", 1),
+                                            setattr(d, "num_kv_heads", 1),
+                                            setattr(d, "seqlen_k", (1 << 23) - 129)),
+     "ATTN_ERR_UNSUPPORTED"),
     ("cu_k without cu_q", lambda d: setattr(d, "cu_seqlens_k", P), "ATTN_ERR_BAD_SHAPE"),
     ("mask kind 7", lambda d: setattr(d, "mask_kind", 7), "ATTN_ERR_BAD_VARIANT"),
     ("mask kind < 0", lambda d: setattr(d, "mask_kind", -1), "ATTN_ERR_BAD_VARIANT"),

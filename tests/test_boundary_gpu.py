@@ -1,6 +1,7 @@
 """GPU behaviour at the C-ABI boundary: strided views in and out, a NULL LSE,
-a non-default stream, bitwise determinism across calls, and no writes outside
-the output rows (guard regions around O and LSE)."""
+a non-default stream, bitwise determinism across calls, no writes outside
+the output rows (guard regions around O and LSE), and the largest slices and
+offsets the 32-bit in-slice addressing allows."""
 import math
 
 import numpy as np
@@ -112,3 +113,69 @@ def test_lse_combines_key_shards():
     err_l = (m - lse).abs().max().item()
     log(f"[boundary] shard merge: max|dO| {err_o:.3e}, max|dLSE| {err_l:.3e}")
     assert err_o <= 2e-2 and err_l <= 1e-3
+
+
+def _tail_case(sq, tail, seed):
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn((sq, 128), generator=g).to(torch.bfloat16)
+    kt = torch.randn((tail, 128), generator=g).to(torch.bfloat16)
+    vt = torch.randn((tail, 128), generator=g).to(torch.bfloat16)
+    return q, kt, vt
+
+
+def _check(o, lse, o_ref, lse_ref, label):
+    err_o = float(np.abs(o.float().cpu().numpy() - o_ref).max())
+    err_l = float(np.abs(lse.cpu().numpy().astype(np.float64) - lse_ref).max())
+    log(f"[boundary] {label}: max|dO| {err_o:.3e}, max|dLSE| {err_l:.3e}")
+    assert err_o <= 2e-2 and err_l <= 1e-3
+
+
+def test_largest_slice():
+    """One head whose K/V slice is the largest the host accepts (its last byte
+    just below 2^31 with one tile of padding): 128 queries bottom-right aligned
+    against 8,388,478 keys under a 200-key causal window, so only keys at the
+    very end of the slice are visible. Every other key is zero; the oracle
+    runs on the last 4096 keys, which bottom-right alignment makes the same
+    problem."""
+    sk, sq, tail, wl = (1 << 23) - 130, 128, 4096, 200
+    q, kt, vt = _tail_case(sq, tail, 41)
+    k = torch.zeros((1, 1, sk, 128), dtype=torch.bfloat16, device=DEV)
+    v = torch.zeros((1, 1, sk, 128), dtype=torch.bfloat16, device=DEV)
+    k[0, 0, sk - tail:] = kt.to(DEV)
+    v[0, 0, sk - tail:] = vt.to(DEV)
+    log(f"[boundary] largest slice: Sk={sk} ({2 * sk * 128 * 2 / 2**30:.2f} GiB of K/V)")
+    o, lse = attn.fwd(q.view(1, 1, sq, 128).to(DEV), k, v, window=(wl, 0), scale=128 ** -0.5)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = oracle.attention(q.view(1, 1, sq, 128), kt.view(1, 1, tail, 128),
+                                      vt.view(1, 1, tail, 128), scale=128 ** -0.5,
+                                      mask=MASK_SLIDING_WINDOW, window_left=wl, window_right=0)
+    _check(o, lse, o_ref, lse_ref, "largest slice")
+    del k, v
+    torch.cuda.empty_cache()
+
+
+def test_sequence_beyond_2gib():
+    """Packed batch whose third sequence starts 2.3 GB into K and V (the
+    first two have 4,500,000 keys each and no queries): the slice base is
+    formed with 64-bit arithmetic, offsets inside a slice stay 32-bit."""
+    n0, sq, tail = 9_000_000, 200, 300
+    q, kt, vt = _tail_case(sq, tail, 42)
+    tk = n0 + tail
+    k = torch.zeros((tk, 1, 128), dtype=torch.bfloat16, device=DEV)
+    v = torch.zeros((tk, 1, 128), dtype=torch.bfloat16, device=DEV)
+    k[n0:, 0] = kt.to(DEV)
+    v[n0:, 0] = vt.to(DEV)
+    cuq = torch.tensor([0, 0, 0, sq], dtype=torch.int32)
+    cuk = torch.tensor([0, n0 // 2, n0, tk], dtype=torch.int32)
+    log(f"[boundary] sequence at {n0 * 256 / 1e9:.2f} GB into K/V")
+    o, lse = attn.fwd(q.view(sq, 1, 128).to(DEV), k, v, causal=True, cu_seqlens_q=cuq.to(DEV),
+                      cu_seqlens_k=cuk.to(DEV), max_seqlen_q=sq, max_seqlen_k=n0 // 2,
+                      scale=128 ** -0.5)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = oracle.attention(q.view(1, 1, sq, 128), kt.view(1, 1, tail, 128),
+                                      vt.view(1, 1, tail, 128), scale=128 ** -0.5,
+                                      mask=MASK_CAUSAL)
+    _check(o.view(1, sq, 1, 128).permute(0, 2, 1, 3), lse.view(1, 1, sq), o_ref, lse_ref,
+           "sequence beyond 2 GiB")
+    del k, v
+    torch.cuda.empty_cache()
