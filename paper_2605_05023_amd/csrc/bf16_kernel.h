@@ -146,8 +146,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 // lane L writes its bytes 16L..16L+15, which hold (row, chunk) with
 // chunk = physical chunk ^ swizzle(row). Rows of load p are those of load 0
 // plus p * ROWS_PER_LOAD, and the swizzle only sees the row modulo 16, so the
-// per-lane byte offset is the same for every p; the row step goes into the
-// (scalar) buffer descriptor.
+// per-lane byte offset is the same for every p and every tile; the tile's
+// and the load's row steps are a wave-uniform addend.
 template <class T>
 __device__ __forceinline__ uint32_t load_lane_offset(int wave, int lane, int64_t stride)
 {
@@ -171,16 +171,13 @@ __device__ __forceinline__ void issue_load(char* lds_tile, __amdgpu_buffer_rsrc_
         rs, (lds_void*)(lds_tile + (4 * p + wave) * 1024), 16, off, 0, 0, 0);
 }
 
+// All LOADS loads of this wave for one tile.
 template <class T>
 __device__ __forceinline__ void issue_tile(char* lds_tile, __amdgpu_buffer_rsrc_t rs, int j0,
                                            uint32_t row_bytes, uint32_t lane_off, int wave)
 {
 #pragma unroll
-    for (int p = 0; p < T::LOADS; ++p) {
-        const uint32_t off = lane_off + (uint32_t)(j0 + p * T::ROWS_PER_LOAD) * row_bytes;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rs, (lds_void*)(lds_tile + (4 * p + wave) * 1024), 16, off, 0, 0, 0);
-    }
+    for (int p = 0; p < T::LOADS; ++p) issue_load<T>(lds_tile, rs, j0, row_bytes, lane_off, wave, p);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b)
@@ -244,12 +241,13 @@ struct Bool {
 // With hp heads per workgroup (32 * 4 / hp rows), the hp query tiles of one
 // 128-row span of a head set have consecutive ids, so they start together
 // on one XCD and read the same K/V tiles at about the same time.
-// Within an XCD the kv-head groups are taken `chunk` at a time (every query
-// head and query tile of the chunk, longest-first inside it), so the K/V
-// tiles in use at any moment belong to a few groups and stay in that XCD's
-// L2 instead of cycling every group's K/V through the caches once per tile. Mode 1 keeps all query heads of a kv-head group on one
-// XCD (workgroup ids are dealt round-robin over the 8 XCDs), so their K/V
-// tiles are shared through that XCD's L2.
+// Mode 1 keeps all query heads of a kv-head group on one XCD (workgroup ids
+// are dealt round-robin over the 8 XCDs), so their K/V tiles are shared
+// through that XCD's L2. Within an XCD the kv-head groups are taken `chunk`
+// at a time (every head set and query tile of the chunk, longest-first
+// inside it), so the K/V tiles in use at any moment belong to a few groups
+// and stay in the L2 instead of cycling every group's K/V through the
+// caches once per tile.
 __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
 {
     // every divisor is launch-invariant: multiply-high and shift (fastdiv.h)

@@ -47,6 +47,12 @@ SMALL = [
     W("bf16_d128_window_wide", "bf16", 1, 2, 2, 260, 128, WINDOW, 1023, 0),
     W("bf16_d128_gqa4_causal", "bf16", 2, 8, 2, 200, 128, CAUSAL),
     W("bf16_d128_gqa8_window", "bf16", 1, 8, 1, 400, 128, WINDOW, 100, 0),
+    # group sizes 3 (one head per workgroup), 6 (two of three head pairs) and
+    # 16 (four sets of four heads), across the workgroup-order modes (B*Hkv a
+    # multiple of 8 or not)
+    W("bf16_d128_gqa3_causal", "bf16", 2, 6, 2, 290, 128, CAUSAL),
+    W("bf16_d64_gqa6_window", "bf16", 4, 12, 2, 211, 64, WINDOW, 50, 0),
+    W("bf16_d128_gqa16_causal", "bf16", 8, 16, 1, 150, 128, CAUSAL),
     W("bf16_d64_alibi_softcap", "bf16", 2, 4, 4, 300, 64, alibi=True, softcap=50.0, sigma=1.5),
     W("bf16_d128_alibi_softcap", "bf16", 1, 4, 2, 260, 128, alibi=True, softcap=20.0, sigma=1.5),
     W("bf16_d64_softcap_small_c", "bf16", 1, 2, 2, 200, 64, softcap=2.0, sigma=1.5),
@@ -80,6 +86,8 @@ VARLEN = [
     ("bf16_d128_window", "bf16", 4, 1, 128, WINDOW, 50, 0, False, 0.0, [300, 70, 128]),
     ("fp32_d128_causal", "fp32", 4, 2, 128, CAUSAL, -1, -1, False, 0.0, [65, 1, 130]),
     ("bf16_all_empty_but_one", "bf16", 2, 2, 128, CAUSAL, -1, -1, False, 0.0, [0, 0, 17, 0]),
+    ("bf16_d128_gqa6_causal", "bf16", 12, 2, 128, CAUSAL, -1, -1, False, 0.0,
+     [33, 200, 1, 129, 64, 0, 97, 150]),
 ]
 
 
