@@ -759,6 +759,17 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int li = lane & 31, lh = lane >> 5;
 
+    // Read the kernel arguments the set-up needs in one round of scalar loads
+    // (the branches below would otherwise spread them over several).
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::"s"(p.map_mode), "s"(p.hp_shift), "s"(p.num_q_tiles), "s"(p.q_order),
+                 "s"(p.div_bh.mul), "s"(p.div_bh.shift), "s"(p.div_bh.d), "s"(p.div_hq.mul),
+                 "s"(p.div_hq.shift), "s"(p.div_hq.d), "s"(p.div_group.mul),
+                 "s"(p.div_group.shift), "s"(p.div_group.d), "s"(p.div_hkv.mul),
+                 "s"(p.div_hkv.shift), "s"(p.div_hkv.d), "s"(p.cu_q), "s"(p.seqlen_q),
+                 "s"(p.seqlen_k), "s"(p.wg_rows), "s"(p.q), "s"(p.k), "s"(p.v), "s"(p.o),
+                 "s"(p.sq_b), "s"(p.sq_h), "s"(p.sq_s), "s"(p.sk_b), "s"(p.sk_h), "s"(p.sk_s),
+                 "s"(p.sv_b), "s"(p.sv_h), "s"(p.sv_s), "s"(p.so_h), "s"(p.so_s));
     const WorkItem it = decode_block(p, blockIdx.x);
     int lq, lk;
     int64_t qrow0 = 0, krow0 = 0;  // first token of the sequence (varlen)
