@@ -99,6 +99,10 @@ struct Traits {
     // softmax without score mods whose rows all see the first visited tile
     // (no left bound): running max checked through the row sums
     static constexpr bool MAXFREE = SOFTMAX && !MODS && !LEFT;
+    // softmax on the general (index-mask) path: O is normalised by the sum of
+    // P as rounded to bf16 (rows there often see only a few keys, where the
+    // rounding of the largest P would show in O)
+    static constexpr bool PSUM_BF16 = SOFTMAX && GEN;
     static constexpr int NB = BN / 32;                   // 32-key blocks per tile
     static constexpr int ROWB = D * 2;                   // bytes per K/V row in LDS
     static constexpr int TILE = BN * ROWB;               // bytes per K or V tile
@@ -187,6 +191,15 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b)
     v[0] = (__bf16)a;
     v[1] = (__bf16)b;
     return __builtin_bit_cast(uint32_t, v);
+}
+
+// a + b of the bf16 pair packed in `w`, added to `acc` (one dot product
+// with (1, 1); the products are exact).
+__device__ __forceinline__ float add_bf16_pair(uint32_t w, float acc)
+{
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, acc, false);
 }
 
 // Lanes l and l ^ 32 hold the two halves of the same query row.
@@ -295,6 +308,7 @@ struct WaveState {
     f32x16 oacc[T::DBLK];      // O^T accumulator
     f32x16 sa[T::NB], sb[T::NB];  // scores of tiles of even / odd parity
     float m_run, l_run;           // softmax only: running max (units) and partial row sum
+    float l_o;                    // softmax only: partial row sum of P as rounded to bf16
     float alpha;                  // softmax with mods: rescale factor of O and l
     bool need;                    // softmax with mods: O and l must be rescaled
     // row constants: visible keys j < pfx (general path) and jlo <= j <= jhi;
@@ -439,6 +453,7 @@ __device__ __forceinline__ void rescale_if_needed(WaveState<T>& ws)
     if constexpr (!T::SOFTMAX || T::MAXFREE) return;
     if (__builtin_amdgcn_ballot_w64(ws.need)) {
         ws.l_run *= ws.alpha;
+        ws.l_o *= ws.alpha;
 #pragma unroll
         for (int d = 0; d < T::DBLK; ++d)
 #pragma unroll
@@ -455,13 +470,24 @@ __device__ __forceinline__ bool row_sees_tile(const WaveState<T>& ws, int jc)
     return band;
 }
 
+// This lane's partial row sums of a tile's P: f in fp32 (the softmax
+// denominator) and, with PSUM_BF16, b of P as rounded to bf16, the values the
+// P V product multiplies, which then normalises O. With the running max
+// behind the row max (lazily updated, or not at all on the check-free path),
+// the largest P of a row is not 1, and its bf16 rounding error (up to 2^-8
+// relative) passes into O unmatched by an fp32 denominator: visible in rows
+// that see few keys.
+struct RowSums {
+    float f, b;
+};
+
 // P = Norm(S) as bf16 B operands of the P V product; returns (softmax) this
-// lane's partial row sum.
+// lane's partial row sums.
 template <class T>
-__device__ __forceinline__ float exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2],
-                                          float m_use, float scale_u)
+__device__ __forceinline__ RowSums exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2],
+                                            float m_use, float scale_u)
 {
-    float rs = 0.0f;
+    RowSums rs = {0.0f, 0.0f};
 #pragma unroll
     for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
@@ -470,11 +496,12 @@ __device__ __forceinline__ float exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw)[
             for (int q = 0; q < 4; ++q) {
                 float p0 = norm_value<T>(s[b][8 * u + 2 * q], m_use, scale_u);
                 float p1 = norm_value<T>(s[b][8 * u + 2 * q + 1], m_use, scale_u);
-                if constexpr (T::SOFTMAX) {
-                    rs += p0;
-                    rs += p1;
-                }
                 pw[b][u][q] = pack_bf16(p0, p1);
+                if constexpr (T::SOFTMAX) {
+                    rs.f += p0;
+                    rs.f += p1;
+                }
+                if constexpr (T::PSUM_BF16) rs.b = add_bf16_pair(pw[b][u][q], rs.b);
             }
         }
     }
@@ -493,15 +520,16 @@ __device__ __forceinline__ float exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw)[
 // tile.
 template <class T>
 __device__ __forceinline__ void check_tile(WaveState<T>& ws, const f32x16 (&s)[T::NB],
-                                           u32x4 (&pw)[T::NB][2], float rs, const AttnParams& p,
+                                           u32x4 (&pw)[T::NB][2], RowSums rs, const AttnParams& p,
                                            int jc)
 {
     if constexpr (!T::SOFTMAX) return;
     if constexpr (!T::MAXFREE) {
-        ws.l_run += rs;
+        ws.l_run += rs.f;
+        ws.l_o += rs.b;
         return;
     }
-    bool need = rs > PSUM_BOUND;
+    bool need = rs.f > PSUM_BOUND;
     if (ws.m_run == -__builtin_inff()) need = need || row_sees_tile(ws, jc);
     if (__builtin_amdgcn_ballot_w64(need)) {
         const bool need_row = pair_max(need ? 1.0f : 0.0f) > 0.0f;
@@ -518,13 +546,15 @@ __device__ __forceinline__ void check_tile(WaveState<T>& ws, const f32x16 (&s)[T
             need_row && m_old != -__builtin_inff() ? __builtin_amdgcn_exp2f(m_old - m_new) : 1.0f;
         ws.m_run = m_new;
         ws.l_run *= alpha;
+        ws.l_o *= alpha;
 #pragma unroll
         for (int d = 0; d < T::DBLK; ++d)
 #pragma unroll
             for (int e = 0; e < 16; ++e) ws.oacc[d][e] *= alpha;
         rs = exp_tile<T>(s, pw, m_new == -__builtin_inff() ? 0.0f : m_new, p.scale_u);
     }
-    ws.l_run += rs;
+    ws.l_run += rs.f;
+    ws.l_o += rs.b;
 }
 
 // O^T += V^T P^T for the V tile in LDS at `vt`.
@@ -584,7 +614,8 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     u32x4 pw[NB][2];
     bf16x8 kop[QK];
     s16x4 vlo[PV], vhi[PV];
-    float rs = 0.0f, mx = -__builtin_inff();
+    RowSums rs = {0.0f, 0.0f};
+    float mx = -__builtin_inff();
 
     auto read_k = [&](int i) __attribute__((always_inline)) {
         const int b = i / T::KSTEPS, t = i % T::KSTEPS;
@@ -614,11 +645,12 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             constexpr int el = i * EQ + 2 * kc.value, bb = el / 16, e = el % 16;
             const float p0 = norm_value<T>(sc[bb][e], m_use, p.scale_u);
             const float p1 = norm_value<T>(sc[bb][e + 1], m_use, p.scale_u);
-            if constexpr (T::SOFTMAX) {
-                rs += p0;
-                rs += p1;
-            }
             pw[bb][e / 8][(e % 8) / 2] = pack_bf16(p0, p1);
+            if constexpr (T::SOFTMAX) {
+                rs.f += p0;
+                rs.f += p1;
+            }
+            if constexpr (T::PSUM_BF16) rs.b = add_bf16_pair(pw[bb][e / 8][(e % 8) / 2], rs.b);
         });
         __builtin_amdgcn_sched_barrier(0);
     });
@@ -663,7 +695,7 @@ __device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, f
     // under causal-like masks): P is zero, nothing to add.
     if (!__builtin_amdgcn_ballot_w64(row_sees_tile(ws, jc))) return;
     u32x4 pw[T::NB][2];
-    const float rs = exp_tile<T>(sc, pw, m_use, p.scale_u);
+    const RowSums rs = exp_tile<T>(sc, pw, m_use, p.scale_u);
     check_tile<T>(ws, sc, pw, rs, p, jc);
     pv_tile<T>(vread, pw, ws);
 }
@@ -900,6 +932,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     for (int d = 0; d < T::DBLK; ++d) ws.oacc[d] = f32x16{};
     ws.m_run = -__builtin_inff();
     ws.l_run = 0.0f;
+    ws.l_o = 0.0f;
     ws.alpha = 1.0f;
     ws.need = false;
 
@@ -1023,14 +1056,16 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             last_step<T>(lds_v0, ws, ws.sa, p, m_use, tile_of(j) * BN);
     }
 
-    // Epilogue. Softmax: O = O^T / l, LSE = (m + log2 l) ln 2 (+ the relative
-    // position shift); lane halves hold halves of the row sum. ReLU / Sigmoid:
-    // O = O^T / L.
+    // Epilogue. Softmax: O = O^T / l (with PSUM_BF16 the sum of the bf16 P
+    // O was made from), LSE = (m + log2 l) ln 2 with the fp32 l (+ the relative
+    // position shift); lane halves hold halves of the row sums. ReLU /
+    // Sigmoid: O = O^T / L.
     float inv = 0.0f;
     float l_tot = 0.0f;
     if constexpr (T::SOFTMAX) {
         l_tot = pair_sum(ws.l_run);
-        inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+        const float lo_tot = T::PSUM_BF16 ? pair_sum(ws.l_o) : l_tot;
+        inv = l_tot > 0.0f && lo_tot > 0.0f ? 1.0f / lo_tot : 0.0f;
     } else {
         inv = lk > 0 ? 1.0f / (float)lk : 0.0f;
     }
