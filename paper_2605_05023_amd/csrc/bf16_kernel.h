@@ -99,10 +99,13 @@ struct Traits {
     // softmax without score mods whose rows all see the first visited tile
     // (no left bound): running max checked through the row sums
     static constexpr bool MAXFREE = SOFTMAX && !MODS && !LEFT;
-    // softmax on the general (index-mask) path: O is normalised by the sum of
-    // P as rounded to bf16 (rows there often see only a few keys, where the
-    // rounding of the largest P would show in O)
-    static constexpr bool PSUM_BF16 = SOFTMAX && GEN;
+    // softmax with soft-cap or ALiBi, or on the general (index-mask) path: O
+    // is normalised by the sum of P as rounded to bf16 (ALiBi makes rows
+    // local, index masks leave some rows few keys; there the rounding of a
+    // row's largest P would show in O). The relative position term alone
+    // makes a row's first visible key its largest, and that key's tile sets
+    // the running max exactly.
+    static constexpr bool PSUM_BF16 = SOFTMAX && (SOFTCAP || BIAS_ == kBiasAlibi || GEN);
     static constexpr int NB = BN / 32;                   // 32-key blocks per tile
     static constexpr int ROWB = D * 2;                   // bytes per K/V row in LDS
     static constexpr int TILE = BN * ROWB;               // bytes per K or V tile
