@@ -1,8 +1,8 @@
 """GPU parity on seeded random variant combinations.
 
-Forty-eight configurations drawn once from a fixed seed: dtype, head dim,
-batch, group size and kv heads, length (fixed or packed varlen), every mask
-kind with random bounds, ALiBi, the relative position term, soft-cap values
+Three batches of 48 configurations, each drawn once from a fixed seed:
+dtype, head dim, batch, group size and kv heads, length (fixed or packed
+varlen), every mask kind with random bounds, ALiBi, the relative position term, soft-cap values
 on both sides of the short form's limit, and the three normalisations. Each
 compares every output element with the CPU oracle at the bars of the other
 parity tests. They exercise combinations no hand-written case lists
@@ -57,7 +57,7 @@ def _draw_cases(n=48, seed=2605):
         relpos = rng.random() < 0.15
         softcap = float(rng.choice([0.0] * 6 + [5.0, 30.0, 50.0, 300.0, 1e4]))
         sigma = 1.5 if (alibi or softcap) else 1.0
-        name = (f"r{i:02d}_{dtype}_d{D}_g{group}x{hkv}_b{B}_{'varlen' if varlen else f's{S}'}"
+        name = (f"s{seed}_r{i:02d}_{dtype}_d{D}_g{group}x{hkv}_b{B}_{'varlen' if varlen else f's{S}'}"
                 f"_{MASK_NAMES[mask]}{'_alibi' if alibi else ''}{'_relpos' if relpos else ''}"
                 f"{f'_cap{softcap:g}' if softcap else ''}{'' if norm == 'softmax' else '_' + norm}")
         wl = Workload(name, dtype, B, hq, hkv, 0 if varlen else S, D, mask=mask, alibi=alibi,
@@ -68,7 +68,7 @@ def _draw_cases(n=48, seed=2605):
     return cases
 
 
-CASES = _draw_cases()
+CASES = _draw_cases(48, 2605) + _draw_cases(48, 7) + _draw_cases(48, 11)
 
 
 @pytest.mark.parametrize("wl", CASES, ids=[w.name for w in CASES])
