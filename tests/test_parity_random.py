@@ -2,12 +2,12 @@
 
 Three batches of 48 configurations, each drawn once from a fixed seed:
 dtype, head dim, batch, group size and kv heads, length (fixed or packed
-varlen), every mask kind with random bounds, ALiBi, the relative position term, soft-cap values
-on both sides of the short form's limit, and the three normalisations. Each
-compares every output element with the CPU oracle at the bars of the other
-parity tests. They exercise combinations no hand-written case lists
-(head-set packing with window and prefix masks, varlen with the index masks,
-soft-cap with ReLU, ...).
+varlen), every mask kind with random bounds, ALiBi, the relative position
+term, soft-cap values on both sides of the short form's limit, and the three
+normalisations. Each compares every output element with the CPU oracle at
+the bars of the other parity tests. They exercise combinations no
+hand-written case lists (head-set packing with window and prefix masks,
+varlen with the index masks, soft-cap with ReLU, ...).
 """
 import numpy as np
 import pytest
