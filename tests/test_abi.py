@@ -117,6 +117,9 @@ CASES = [
                                             setattr(d, "seqlen_k", (1 << 23) - 129)),
      "ATTN_ERR_UNSUPPORTED"),
     ("cu_k without cu_q", lambda d: setattr(d, "cu_seqlens_k", P), "ATTN_ERR_BAD_SHAPE"),
+    ("grid beyond int32", lambda d: (setattr(d, "batch", 1 << 21), setattr(d, "num_q_heads", 1 << 10),
+                                     setattr(d, "num_kv_heads", 1 << 10), setattr(d, "seqlen_q", 1),
+                                     setattr(d, "seqlen_k", 1)), "ATTN_ERR_UNSUPPORTED"),
     ("mask kind 7", lambda d: setattr(d, "mask_kind", 7), "ATTN_ERR_BAD_VARIANT"),
     ("mask kind < 0", lambda d: setattr(d, "mask_kind", -1), "ATTN_ERR_BAD_VARIANT"),
     ("norm kind 3", lambda d: setattr(d, "norm_kind", 3), "ATTN_ERR_BAD_VARIANT"),
