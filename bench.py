@@ -143,10 +143,18 @@ def cpu_baseline(inp, flops_per_row_fn, min_seconds: float, max_seconds: float, 
         if elapsed + 2 * dt > max_seconds:
             break
         batch = min(batch * 2, 16384)
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f
+                              if ln.startswith("model name")), None)
+    except OSError:
+        pass
     return {
         "value": flops / elapsed / 1e12,
         "unit": "TFLOP/s",
         "cores": oracle.num_threads(),
+        "cpu_model": cpu_model,
         "kind": "oracle",
         "sample": f"{done} of {total_rows} query rows (seeded random), fp64 dense "
                   f"materialised scores, {elapsed:.1f} s; unit counts unmasked FLOPs of the "
