@@ -273,10 +273,10 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.q_order = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.num_global > 0 ? 1 : 0;
     // Keep each kv-head group on one XCD when the groups divide evenly. The
     // longest-first order over all groups balances best and is kept while
-    // the K/V of all groups fit the 256 MB Infinity Cache with room to spare;
-    // beyond that (measured: 537 MB of K/V, 1.39x faster chunked) the groups
-    // of an XCD are walked in chunks holding at least one round of its
-    // workgroup slots (32 CUs x 2), so the live K/V stays cached.
+    // the K/V of all groups fill at most half of the 256 MB Infinity Cache;
+    // beyond that (measured: 537 MB of K/V 1.39x and 254 MB 1.03x faster
+    // chunked) the groups of an XCD are walked in chunks holding at least one
+    // round of its workgroup slots (32 CUs x 2), so the live K/V stays cached.
     p.map_mode = ((int64_t)d.batch * d.num_kv_heads) % 8 == 0 ? 1 : 0;
     {
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
@@ -284,7 +284,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         const int64_t kv_bytes = kv_tokens * d.num_kv_heads * D * elt * 2;
         const int64_t per_group = (int64_t)(p.group / hp) * q_tiles;  // workgroups of a kv group
         int64_t chunk = groups_per_xcd;
-        if (kv_bytes > (int64_t)320 << 20) chunk = (64 + per_group - 1) / per_group;
+        if (kv_bytes > (int64_t)128 << 20) chunk = (64 + per_group - 1) / per_group;
         if (chunk > groups_per_xcd) chunk = groups_per_xcd;
         p.chunk = (int32_t)(chunk > 0 ? chunk : 1);
     }
