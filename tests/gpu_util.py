@@ -18,7 +18,7 @@ LSE_TOL = 1e-3
 # ReLU / Sigmoid outputs are sums scaled by 1/L, of order 1/sqrt(L), so an
 # absolute bar would not test them: their error must stay within the same
 # fraction of the output's own scale, max|dO| <= O_TOL * max|O_ref|. The
-# arithmetic allows it: P is rounded to bf16 (relative 2^-9) and O to its dtype.
+# arithmetic allows it: P is rounded to bf16 (relative 2^-8 at most) and O to its dtype.
 
 
 def gpu_available() -> bool:
