@@ -386,8 +386,8 @@ __device__ __forceinline__ void qk_tile(const char* kt, const WaveState<T>& ws, 
         }
     }
     // Issue order: K reads AHEAD products ahead, then one product and one read
-    // at a time, so each accumulation chain runs back to back (a product that
-    // depends on the one two before it would stall).
+    // at a time, block by block (each accumulation chain back to back: faster
+    // than the compiler's own interleaving of the two chains).
     constexpr int N = T::NB * T::KSTEPS, AHEAD = 4;
     __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);  // DS read
 #pragma unroll
@@ -593,10 +593,8 @@ __device__ __forceinline__ void pv_tile(const char* vt, const u32x4 (&pw)[T::NB]
 // transpose reads of a later MFMA and a share of the score mods, mask and max
 // of S_next. A scheduling barrier after every slice keeps this order, so the
 // vector work runs while the matrix cores are busy and LDS latency stays
-// hidden. The QK^T products run block by block: each accumulation chain is
-// issued back to back (a product that depends on the one just before it
-// issues without waiting for its result, one that depends on the one two
-// before stalls).
+// hidden. The QK^T products run block by block, each accumulation chain
+// issued back to back, the order that measured fastest.
 template <class T, bool MASKED, class LOADER>
 __device__ __forceinline__ void pipelined_step(const char* kread, const char* vread,
                                                WaveState<T>& ws, const f32x16 (&sc)[T::NB],
