@@ -200,7 +200,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one MI355X "
+        print(f"bench.py: --gpus {args.gpus} is not supported: the benchmark measures one MI355X "
               f"(the kernel on one GPU's share); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
