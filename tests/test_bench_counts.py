@@ -44,3 +44,31 @@ def test_headline_pair_counts():
     assert bench.visible_pairs(make_inputs(WORKLOADS["causal_bf16"])) == 2048 * 2049 // 2 * 64
     assert bench.visible_pairs(make_inputs(WORKLOADS["gqa_swa_bf16"])) == \
         sum(min(i + 1, 1024) for i in range(8192)) * 64
+
+
+TRAFFIC = sorted(f[len("traffic_"):-3] for f in os.listdir(bench.PROFILES)
+                 if f.startswith("traffic_") and f.endswith(".md"))
+
+
+def _field(text, key):
+    import re
+    m = re.search(rf"{key}:\s*([0-9a-fA-F.eE+]+)", text)
+    assert m, key
+    return m.group(1)
+
+
+@pytest.mark.parametrize("name", TRAFFIC)
+def test_traffic_summary(name):
+    """Each committed HBM-traffic summary names a workload, states no fewer
+    bytes than the method must move, and is used by bench.py only while its
+    kernel-source hash is the current one."""
+    assert name in WORKLOADS
+    text = open(os.path.join(bench.PROFILES, f"traffic_{name}.md")).read()
+    hbm = float(_field(text, "hbm_bytes_per_launch"))
+    alg = int(_field(text, "algorithmic_bytes_per_launch"))
+    assert hbm >= 0.9 * alg
+    if name == "causal_bf16":
+        assert alg == bench.algorithmic_bytes(make_inputs(WORKLOADS[name]))
+    stored = _field(text, "kernel_hash")
+    current = bench.kernel_hash()
+    assert bench.read_traffic(name) == (hbm if stored == current else None)
