@@ -335,16 +335,18 @@ def pin_row_subset(lib):
     assert np.isnan(np.delete(ls.reshape(-1), rows)).all()
 
 
-def _zero_q_counts(lib, S, visible_sets, what, **kw):
+def _zero_q_counts(lib, S, visible_sets, what, sq=None, **kw):
     """Q = 0: O_i = mean of the visible V rows, LSE_i = ln n_i (O = 0, LSE = -inf
-    for an empty row). visible_sets[i] is the set of keys row i must see."""
+    for an empty row). visible_sets[i] is the set of keys row i must see; with
+    sq < S there are sq queries against S keys."""
     D = 3
+    sq = S if sq is None else sq
     v = _rand((1, 1, S, D), 40)
-    q = torch.zeros((1, 1, S, D))
+    q = torch.zeros((1, 1, sq, D))
     k = _rand((1, 1, S, D), 41)
     o, lse = oracle.attention(q, k, v, scale=1.0, lib=lib, **kw)
     vn = v[0, 0].double().numpy()
-    for i in range(S):
+    for i in range(sq):
         js = sorted(visible_sets[i])
         if not js:
             _close(o[0, 0, i], np.zeros(D), 0.0, f"{what}: empty row {i} O")
@@ -390,6 +392,17 @@ def pin_relative_position(lib):
     for i in range(S):
         z = sum(e ** (i - j) for j in range(S))
         _close(lse[0, 0, i], math.log(z), 1e-12, f"relpos Z row {i}")
+    # the term is added after the soft-cap: with Q = 0 the capped score is
+    # C tanh(0) = 0 for any C, so the weights stay e^(i-j) (capping the sum
+    # would give e^(C tanh((i-j)/C)))
+    for cap in (0.5, 2.0):
+        o, lse = oracle.attention(q, k, v, scale=1.0, mask=oracle.MASK_CAUSAL, relpos=True,
+                                  softcap=cap, lib=lib)
+        for i in range(S):
+            z = (e ** (i + 1) - 1) / (e - 1)
+            _close(lse[0, 0, i], math.log(z), 1e-12, f"relpos after cap {cap} Z row {i}")
+            _close(o[0, 0, i], [e ** (i - j) / z if j <= i else 0.0 for j in range(S)], 1e-12,
+                   f"relpos after cap {cap} O row {i}")
     # bottom-right alignment: 3 queries against 7 keys, query i at position i + 4
     o, lse = oracle.attention(q[:, :, 4:], k, v, scale=1.0, mask=oracle.MASK_CAUSAL,
                               relpos=True, lib=lib)
@@ -509,11 +522,206 @@ def pin_causal_blockwise(lib):
         _close(lb, lc, 0.0, f"blockwise reduction LSE (Lq={lq_})")
 
 
+def _visible_sets(kind, sq, sk, *, wl=-1, wr=-1, lp=0, G=(), ids=None, lq_=0):
+    """Keys visible to each of sq queries against sk keys, written from the
+    paper's case analyses at the key-axis position i' = i + sk - sq."""
+    sets = []
+    for i in range(sq):
+        ii = i + sk - sq
+        keys = range(sk)
+        if kind == oracle.MASK_NONE:
+            vis = set(keys)
+        elif kind == oracle.MASK_CAUSAL:
+            vis = {j for j in keys if j <= ii}
+        elif kind == oracle.MASK_SLIDING_WINDOW:
+            vis = {j for j in keys if (wl < 0 or ii - j <= wl) and (wr < 0 or j - ii <= wr)}
+        elif kind == oracle.MASK_PREFIX_LM:
+            vis = {j for j in keys if j < lp or j <= ii}
+        elif kind == oracle.MASK_GLOBAL_WINDOW:
+            vis = set(keys) if ii in G else \
+                {j for j in keys if abs(ii - j) <= wl or j in G}
+        elif kind == oracle.MASK_SHARE_QUESTION:
+            vis = set() if ii < 0 else {j for j in keys if j <= ii and (
+                (ids[ii] < 0 and ids[j] < 0) or (ids[ii] >= 0 and ids[j] in (-1, ids[ii])))}
+        elif kind == oracle.MASK_CAUSAL_BLOCKWISE:
+            vis = set() if ii < 0 else {j for j in keys if j <= ii and (
+                ii >= lq_ or ids[ii] == ids[j])}
+        else:
+            raise ValueError(kind)
+        sets.append(vis)
+    return sets
+
+
+def pin_bottom_right_counts(lib):
+    """Q = 0 with fewer (and more) queries than keys: every mask kind places
+    query i at key position i' = i + Sk - Sq (O = mean of the visible V rows,
+    LSE = ln n_i; rows with no visible key give O = 0, LSE = -inf)."""
+    S = 13
+    ids_sq = _ids_from_starts(S, [4, 7, 11])
+    ids_bw = _ids_from_starts(S, [0, 3, 8])
+    cases = [
+        (dict(mask=oracle.MASK_CAUSAL), dict()),
+        (dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=2, window_right=0), dict(wl=2, wr=0)),
+        (dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=1, window_right=3), dict(wl=1, wr=3)),
+        (dict(mask=oracle.MASK_PREFIX_LM, prefix_len=3), dict(lp=3)),
+        (dict(mask=oracle.MASK_GLOBAL_WINDOW, window_left=1, window_right=1,
+              global_tokens=[2, 9]), dict(wl=1, G=(2, 9))),
+        (dict(mask=oracle.MASK_SHARE_QUESTION, token_ids=ids_sq), dict(ids=ids_sq)),
+        (dict(mask=oracle.MASK_CAUSAL_BLOCKWISE, token_ids=ids_bw, query_start=10),
+         dict(ids=ids_bw, lq_=10)),
+    ]
+    for kw, skw in cases:
+        for sq in (1, 5, S):
+            sets = _visible_sets(kw["mask"], sq, S, **skw)
+            _zero_q_counts(lib, S, sets, f"Sq={sq} Sk={S} {kw}", sq=sq, **kw)
+    # more queries than keys: the first Sq - Sk rows of a causal mask see nothing
+    for kw, skw in cases[:4]:
+        sk = 6
+        sets = _visible_sets(kw["mask"], 9, sk, **skw)
+        D = 3
+        v = _rand((1, 1, sk, D), 60)
+        o, lse = oracle.attention(torch.zeros((1, 1, 9, D)), _rand((1, 1, sk, D), 61), v,
+                                  scale=1.0, lib=lib, **kw)
+        vn = v[0, 0].double().numpy()
+        for i, vis in enumerate(sets):
+            js = sorted(vis)
+            if not js:
+                _close(o[0, 0, i], np.zeros(D), 0.0, f"Sq>Sk empty row {i} {kw}")
+                _close(lse[0, 0, i], -math.inf, 0.0, f"Sq>Sk empty LSE {i} {kw}")
+            else:
+                _close(o[0, 0, i], vn[js].mean(0), 1e-12, f"Sq>Sk row {i} {kw}")
+                _close(lse[0, 0, i], math.log(len(js)), 1e-12, f"Sq>Sk LSE {i} {kw}")
+
+
+def pin_alibi_bottom_right(lib):
+    """Q = 0, ALiBi, Sq < Sk: query i at position i' = i + Sk - Sq weighs key j by
+    r^|i' - j| (r = e^-m); with V = identity O_i[j] = r^|i'-j| / Z_i, Z_i a
+    two-sided geometric sum (non-causal) or one-sided (causal)."""
+    S, sq, m = 9, 4, 0.37
+    r = math.exp(-m)
+    q = torch.zeros((1, 1, sq, S))
+    k = _rand((1, 1, S, S), 62)
+    v = torch.eye(S).reshape(1, 1, S, S)
+    o, lse = oracle.attention(q, k, v, scale=1.0, slopes=torch.tensor([m]), lib=lib)
+    oc, lc = oracle.attention(q, k, v, scale=1.0, slopes=torch.tensor([m]),
+                              mask=oracle.MASK_CAUSAL, lib=lib)
+    for i in range(sq):
+        ii = i + S - sq
+        z = (1 - r ** (ii + 1)) / (1 - r) + r * (1 - r ** (S - 1 - ii)) / (1 - r)
+        _close(lse[0, 0, i], math.log(z), 1e-6, f"ALiBi Sq<Sk Z row {i}")
+        _close(o[0, 0, i], [r ** abs(ii - j) / z for j in range(S)], 1e-6,
+               f"ALiBi Sq<Sk O row {i}")
+        zc = (1 - r ** (ii + 1)) / (1 - r)
+        _close(lc[0, 0, i], math.log(zc), 1e-6, f"causal ALiBi Sq<Sk Z row {i}")
+        _close(oc[0, 0, i], [r ** (ii - j) / zc if j <= ii else 0.0 for j in range(S)], 1e-6,
+               f"causal ALiBi Sq<Sk O row {i}")
+
+
+def pin_norm_key_length(lib):
+    """ReLU / Sigmoid divide by L = the key length of the row's sequence, also
+    when it differs from the query length: with Q = 0, Sigmoid gives
+    O_i = sum of the visible V rows / (2 Lk)."""
+    D = 3
+    for sq, sk, mask in ((2, 7, oracle.MASK_NONE), (3, 7, oracle.MASK_CAUSAL),
+                         (8, 5, oracle.MASK_CAUSAL)):
+        v = _rand((1, 1, sk, D), 63)
+        o, lse = oracle.attention(torch.zeros((1, 1, sq, D)), _rand((1, 1, sk, D), 64), v,
+                                  scale=1.0, mask=mask, norm=oracle.NORM_SIGMOID, lib=lib)
+        vn = v[0, 0].double().numpy()
+        for i, vis in enumerate(_visible_sets(mask, sq, sk)):
+            js = sorted(vis)
+            want = vn[js].sum(0) / (2 * sk) if js else np.zeros(D)
+            _close(o[0, 0, i], want, 1e-12, f"sigmoid L=Lk sq={sq} sk={sk} row {i}")
+        assert np.isnan(lse).all()
+    # packed sequences with their own query and key lengths
+    lq, lk = [2, 5, 1], [6, 3, 4]
+    cuq = np.concatenate([[0], np.cumsum(lq)]).astype(np.int32)
+    cuk = np.concatenate([[0], np.cumsum(lk)]).astype(np.int32)
+    v = _rand((sum(lk), 1, D), 65)
+    o, _ = oracle.attention(torch.zeros((sum(lq), 1, D)), _rand((sum(lk), 1, D), 66), v,
+                            scale=1.0, mask=oracle.MASK_CAUSAL, norm=oracle.NORM_SIGMOID,
+                            cu_seqlens_q=cuq, cu_seqlens_k=cuk, lib=lib)
+    vn = v[:, 0].double().numpy()
+    for s_, (a, b) in enumerate(zip(lq, lk)):
+        for i, vis in enumerate(_visible_sets(oracle.MASK_CAUSAL, a, b)):
+            js = [cuk[s_] + j for j in sorted(vis)]
+            want = vn[js].sum(0) / (2 * b) if js else np.zeros(D)
+            _close(o[cuq[s_] + i, 0], want, 1e-12, f"varlen sigmoid L=Lk seq {s_} row {i}")
+
+
+_REDUCTION_VARIANTS = [
+    dict(mask=oracle.MASK_NONE),
+    dict(mask=oracle.MASK_CAUSAL),
+    dict(mask=oracle.MASK_SLIDING_WINDOW, window_left=3, window_right=1),
+    dict(mask=oracle.MASK_PREFIX_LM, prefix_len=4),
+    dict(mask=oracle.MASK_GLOBAL_WINDOW, window_left=2, window_right=2, global_tokens=[2, 8]),
+    dict(mask=oracle.MASK_SHARE_QUESTION, token_ids=_ids_from_starts(12, [3, 6, 10])),
+    dict(mask=oracle.MASK_CAUSAL_BLOCKWISE, token_ids=_ids_from_starts(12, [0, 4, 7]),
+         query_start=9),
+]
+_REDUCTION_MODS = [
+    dict(),
+    dict(slopes=[0.3, 0.7, 0.2, 0.9]),
+    dict(relpos=True),
+    dict(softcap=1.5, relpos=True, slopes=[0.5, 0.1, 0.25, 0.05]),
+    dict(norm=oracle.NORM_RELU, slopes=[0.3, 0.7, 0.2, 0.9]),
+    dict(norm=oracle.NORM_SIGMOID, relpos=True, softcap=2.0),
+]
+
+
+def pin_shape_reduction(lib):
+    """Fewer queries than keys is the tail of the square problem: the Sq rows of
+    an Sq x Sk run equal the last Sq rows of the Sk x Sk run on the same keys,
+    for every mask kind, bias, soft-cap and normalisation (fixed length and
+    packed sequences). This is what placing query i at key position
+    i + Sk - Sq means; it fixes that alignment, and L = Lk for ReLU / Sigmoid,
+    in every variant at once."""
+    Sk, Hq, Hkv, D = 12, 4, 2, 5
+    q = _rand((1, Hq, Sk, D), 70, 1.3)
+    k = _rand((1, Hkv, Sk, D), 71, 1.3)
+    v = _rand((1, Hkv, Sk, D), 72)
+    for vk in _REDUCTION_VARIANTS:
+        for mk in _REDUCTION_MODS:
+            kw = dict(vk, **mk)
+            if "slopes" in kw:
+                kw["slopes"] = torch.tensor(kw["slopes"])
+            of, lf = oracle.attention(q, k, v, scale=0.45, lib=lib, **kw)
+            for sq in (1, 5):
+                os_, ls = oracle.attention(q[:, :, Sk - sq:], k, v, scale=0.45, lib=lib, **kw)
+                _close(os_, of[:, :, Sk - sq:], 0.0, f"Sq={sq} tail O {kw}")
+                if kw.get("norm", oracle.NORM_SOFTMAX) == oracle.NORM_SOFTMAX:
+                    _close(ls, lf[:, :, Sk - sq:], 0.0, f"Sq={sq} tail LSE {kw}")
+    # packed: every sequence keeps its last lq_s queries of lk_s
+    lk = [12, 7, 1, 9]
+    lq = [5, 7, 0, 2]
+    T = sum(lk)
+    qp = _rand((T, Hq, D), 73, 1.3)
+    kp = _rand((T, Hkv, D), 74, 1.3)
+    vp = _rand((T, Hkv, D), 75)
+    cuk = np.concatenate([[0], np.cumsum(lk)]).astype(np.int32)
+    cuq = np.concatenate([[0], np.cumsum(lq)]).astype(np.int32)
+    tail = np.concatenate([np.arange(cuk[s + 1] - lq[s], cuk[s + 1]) for s in range(len(lk))])
+    for vk in _REDUCTION_VARIANTS:
+        for mk in _REDUCTION_MODS:
+            kw = dict(vk, **mk)
+            if "slopes" in kw:
+                kw["slopes"] = torch.tensor(kw["slopes"])
+            of, lf = oracle.attention(qp, kp, vp, scale=0.45, cu_seqlens_q=cuk, cu_seqlens_k=cuk,
+                                      lib=lib, **kw)
+            os_, ls = oracle.attention(qp[torch.as_tensor(tail)], kp, vp, scale=0.45,
+                                       cu_seqlens_q=cuq, cu_seqlens_k=cuk, lib=lib, **kw)
+            _close(os_, of[tail], 0.0, f"varlen tail O {kw}")
+            if kw.get("norm", oracle.NORM_SOFTMAX) == oracle.NORM_SOFTMAX:
+                _close(ls, lf[:, tail], 0.0, f"varlen tail LSE {kw}")
+
+
 ALL_PINS = [pin_hand_cases, pin_probability_rows, pin_constant_v, pin_causal_row0,
             pin_single_key_window, pin_zero_query_counts, pin_zero_query_alibi,
             pin_reductions, pin_torch_sdpa, pin_gqa_equals_repeated, pin_varlen_concat,
             pin_varlen_unequal_lengths, pin_row_subset, pin_prefix_lm, pin_relative_position,
-            pin_relu_sigmoid, pin_global_window, pin_share_question, pin_causal_blockwise]
+            pin_relu_sigmoid, pin_global_window, pin_share_question, pin_causal_blockwise,
+            pin_bottom_right_counts, pin_alibi_bottom_right, pin_norm_key_length,
+            pin_shape_reduction]
 
 
 def failing_pins(lib):

@@ -41,8 +41,49 @@ MUTANTS = [
      "if (p->relpos) s += (double)(j - i - (lk - lq));"),
     ("relative position top-left", "if (p->relpos) s += (double)(i + (lk - lq) - j);",
      "if (p->relpos) s += (double)(i - j);"),
-    ("relative position before soft-cap", "if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);",
-     "if (p->relpos) s += (double)(i + (lk - lq) - j);\n    if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);"),
+    # the relative-position line moved in front of the soft-cap (not duplicated)
+    ("relative position before soft-cap",
+     "    if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);\n"
+     "    if (p->slopes) {\n"
+     "        int64_t rel = i + (lk - lq) - j;\n"
+     "        s -= p->slopes[h] * (double)(rel < 0 ? -rel : rel);\n"
+     "    }\n"
+     "    if (p->relpos) s += (double)(i + (lk - lq) - j);\n",
+     "    if (p->relpos) s += (double)(i + (lk - lq) - j);\n"
+     "    if (p->softcap > 0.0) s = p->softcap * tanh(s / p->softcap);\n"
+     "    if (p->slopes) {\n"
+     "        int64_t rel = i + (lk - lq) - j;\n"
+     "        s -= p->slopes[h] * (double)(rel < 0 ? -rel : rel);\n"
+     "    }\n"),
+    # top-left alignment (query i at key position i instead of i + Lk - Lq),
+    # one variant at a time; the window checks of the sliding window (first
+    # occurrence) and of the global sliding window (second) are the same text
+    ("ALiBi top-left", "int64_t rel = i + (lk - lq) - j;", "int64_t rel = i - j;"),
+    ("window top-left",
+     "if (p->window_left >= 0 && ii - j > p->window_left) return 0;\n"
+     "        if (p->window_right >= 0 && j - ii > p->window_right) return 0;",
+     "if (p->window_left >= 0 && i - j > p->window_left) return 0;\n"
+     "        if (p->window_right >= 0 && j - i > p->window_right) return 0;", 0),
+    ("global window band top-left",
+     "if (p->window_left >= 0 && ii - j > p->window_left) return 0;\n"
+     "        if (p->window_right >= 0 && j - ii > p->window_right) return 0;",
+     "if (p->window_left >= 0 && i - j > p->window_left) return 0;\n"
+     "        if (p->window_right >= 0 && j - i > p->window_right) return 0;", 1),
+    ("global rows top-left", "if (in_global(p, ii) || in_global(p, j)) return 1;",
+     "if (in_global(p, i) || in_global(p, j)) return 1;"),
+    ("PrefixLM top-left", "return j <= ii;                  /* causal generation */",
+     "return j <= i;"),
+    ("share question top-left",
+     "if (j > ii || ii < 0) return 0;\n        int32_t idi = p->token_ids[ii], idj = p->token_ids[j];",
+     "if (j > i) return 0;\n        int32_t idi = p->token_ids[i], idj = p->token_ids[j];"),
+    ("causal blockwise top-left",
+     "if (ii >= p->query_start) return 1;          /* test query visibility   */\n"
+     "        return p->token_ids[ii] == p->token_ids[j];",
+     "if (i >= p->query_start) return 1;\n        return p->token_ids[i] == p->token_ids[j];"),
+    ("causal blockwise causal part top-left",
+     "if (j > ii || ii < 0) return 0;\n        if (ii >= p->query_start)",
+     "if (j > i) return 0;\n        if (ii >= p->query_start)"),
+    ("norm L from the query length", "double pj = a / (double)lk;", "double pj = a / (double)lq;"),
     ("norm without 1/L", "double pj = a / (double)lk;", "double pj = a;"),
     ("ReLU passes negatives", "a = s[j] > 0.0 ? s[j] : 0.0;", "a = s[j];"),
     ("Sigmoid sign", "a = 1.0 / (1.0 + exp(-s[j]));", "a = 1.0 / (1.0 + exp(s[j]));"),
@@ -59,11 +100,24 @@ MUTANTS = [
 ]
 
 
-@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_mutant_is_caught(tmp_path, name, old, new):
+def _mutate(src, old, new, nth=None):
+    """Replace every occurrence of `old`, or only the nth (0-based)."""
+    if nth is None:
+        return src.replace(old, new)
+    at = -1
+    for _ in range(nth + 1):
+        at = src.index(old, at + 1)
+    return src[:at] + new + src[at + len(old):]
+
+
+@pytest.mark.parametrize("mutant", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, mutant):
+    name, old, new = mutant[:3]
+    nth = mutant[3] if len(mutant) > 3 else None
     src = open(SRC).read()
-    assert src.count(old) >= 1, f"mutation site for '{name}' not found"
-    mutated = src.replace(old, new)
+    assert src.count(old) > (nth or 0), f"mutation site for '{name}' not found"
+    mutated = _mutate(src, old, new, nth)
+    assert mutated != src
     path = tmp_path / "attn_ref_mutant.c"
     path.write_text(mutated)
     so = oracle.build(str(path), str(tmp_path / "libmutant.so"))
