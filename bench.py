@@ -1,9 +1,12 @@
 """Benchmark of the fused attention forward on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload causal_bf16]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload varlen_gqa_bf16]
 
 A step is one attn_fwd call (the whole fused forward) over one batch of the
-seeded synthetic workload, with inputs already resident in HBM. Prints one
+seeded synthetic workload, with inputs already resident in HBM. The default
+workload is the largest single-GPU configuration: 16 packed causal sequences
+of 256..8192 tokens (61,938 in total) with 32 query and 8 key/value heads of
+dimension 128. Prints one
 JSON line: throughput in TFLOP/s counting only unmasked score entries
 (4 * head_dim FLOPs per visible query/key pair per query head), the roofline
 of the kernel against the bf16 matrix-core peak, and the CPU oracle timed on a
@@ -38,8 +41,11 @@ PEAK_BF16_TFLOPS = 2516.6
 PEAK_FP32_TFLOPS = 157.3
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2605_05023_amd", "csrc")
+# Everything that decides what a launch does: the kernels, the host side that
+# chooses the schedule (heads per workgroup, workgroup order, chunking), and
+# the ABI header.
 KERNEL_SOURCES = sorted(os.path.join("paper_2605_05023_amd", "csrc", f) for f in os.listdir(CSRC)
-                        if f.endswith((".hip", ".h")))
+                        if f.endswith((".hip", ".h", ".cpp"))) + [os.path.join("include", "attn.h")]
 
 
 def row_counts(inp, S: int) -> np.ndarray:
@@ -101,8 +107,10 @@ def kernel_hash() -> str:
 
 
 def read_traffic(workload: str):
-    """HBM bytes per launch from the committed PMC summary, if it was measured on
-    the current kernel sources (else None)."""
+    """Bytes per launch from the committed PMC summary (FETCH_SIZE + WRITE_SIZE,
+    calibrated against a plain copy), if it was measured on the current library
+    sources (else None). The counters count the L2's traffic to the fabric,
+    which includes Infinity Cache hits: an upper bound on HBM bytes."""
     path = os.path.join(PROFILES, f"traffic_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -191,7 +199,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="causal_bf16", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="varlen_gqa_bf16", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="minimum oracle time for the CPU baseline sample")
@@ -324,6 +332,7 @@ def main():
             "kernel_avg_ms": round(kernel_ms, 5),
             "kernel_median_ms": round(warm[len(warm) // 2], 5),
             "kernel_min_ms": round(warm[0], 5),
+            "kernel_max_ms": round(warm[-1], 5),
             "kernel_cold_median_ms": round(cold[len(cold) // 2], 5),
             "algorithmic_bytes": nbytes,
             "algorithmic_gbps": round(nbytes / (kernel_ms * 1e-3) / 1e9, 1),

@@ -28,8 +28,9 @@
  *
  * Errors: every entry point returns ATTN_OK (0) or a negative attn_status_t.
  * Argument validation happens on the host before any HIP call, so a rejected
- * call has no side effect. Device-side preconditions (cu_seqlens contents)
- * are documented per field and are not checked by the kernel.
+ * call has no side effect. Device-side preconditions (the contents of
+ * cu_seqlens, segment_starts and global_tokens) are documented per field and
+ * are not checked by the kernel; ATTN_FLAG_VALIDATE checks them on the host.
  *
  * Concurrency: no global mutable state; calls on different streams may run
  * concurrently. The device used is the caller's current HIP device.
@@ -43,10 +44,22 @@
 extern "C" {
 #endif
 
-#define ATTN_ABI_VERSION 2
+#define ATTN_ABI_VERSION 3
 
-/* Largest attn_variant_desc.num_segments (segments are staged on chip). */
+/* Largest attn_variant_desc.num_segments, and num_global when global_tokens
+ * lists the global positions (both are staged on chip). */
 #define ATTN_MAX_SEGMENTS 2048
+
+/*
+ * attn_variant_desc.flags bits.
+ * ATTN_FLAG_VALIDATE: before the launch, copy cu_seqlens_q / cu_seqlens_k,
+ *   segment_starts and global_tokens to the host (waiting for desc->stream)
+ *   and check the device-side preconditions documented on those fields;
+ *   a violation returns ATTN_ERR_BAD_SHAPE (cu_seqlens) or
+ *   ATTN_ERR_BAD_VARIANT (segments, global positions) and nothing is
+ *   enqueued. A debugging aid: it costs a host round trip per call.
+ */
+#define ATTN_FLAG_VALIDATE 1u
 
 typedef enum attn_dtype {
     ATTN_BF16 = 0, /* q, k, v, out are bfloat16; accumulation in fp32 */
@@ -67,8 +80,9 @@ typedef enum attn_dtype {
  *   GLOBAL_SLIDING_WINDOW : i' - j <= window_left and j - i' <= window_right
  *                    (the paper's |i - j| <= w is window_left = window_right
  *                    = w), or i' in G, or j in G, where the global set G is
- *                    positions 0 .. num_global-1 (Appendix A "Global Sliding
- *                    Window").
+ *                    the num_global positions listed in global_tokens, or
+ *                    positions 0 .. num_global-1 when global_tokens is NULL
+ *                    (Appendix A "Global Sliding Window").
  *   SHARE_QUESTION : positions before segment_starts[0] are the prompt Q;
  *                    segment k (positions segment_starts[k] up to the next
  *                    start, the last one up to the end) is response A_k.
@@ -174,6 +188,22 @@ typedef struct attn_variant_desc {
                                     >= 0; positions are per sequence (varlen)     */
     int32_t num_segments;        /* 1 .. ATTN_MAX_SEGMENTS for those kinds         */
     int32_t query_start;         /* CAUSAL_BLOCKWISE: L_q >= 0                      */
+    const int32_t *global_tokens; /* GLOBAL_SLIDING_WINDOW: device int32
+                                    [num_global] key positions of G, strictly
+                                    increasing and >= 0 (per sequence when
+                                    varlen; positions past a sequence's end are
+                                    ignored), num_global <= ATTN_MAX_SEGMENTS; or
+                                    NULL for G = positions 0 .. num_global-1      */
+    uint32_t flags;              /* ATTN_FLAG_* bits                               */
+    /* Workgroup schedule overrides for tuning and tests (0 = the library's
+       choice); they change the order of the work, never the result.          */
+    int32_t sched_heads_per_wg;  /* bf16: query heads of one kv group per
+                                    workgroup, 1, 2 or 4, dividing Hq / Hkv       */
+    int32_t sched_order;         /* 1: natural order; 2: every kv group on one
+                                    XCD (needs batch * Hkv a multiple of 8)      */
+    int32_t sched_chunk;         /* with sched_order 2 (or the library choosing
+                                    it): kv groups walked per chunk within an XCD,
+                                    1 .. batch * Hkv / 8                          */
 } attn_variant_desc;
 
 /*

@@ -4,6 +4,10 @@
 `attn_variant_desc` and calls `attn_fwd` of libattn.so. The computation runs
 entirely in the library's HIP kernels; if the library is missing the import
 of `fwd`'s backend fails loudly.
+
+The C ABI sees only pointers, so every shape is checked here against q before
+the call: a mismatch raises ValueError (TypeError for a dtype or device) and
+nothing is launched.
 """
 from __future__ import annotations
 
@@ -13,17 +17,17 @@ from typing import Optional
 
 import torch
 
-from ._abi import (ATTN_BF16, ATTN_FP32, ATTN_MASK_CAUSAL, ATTN_MASK_CAUSAL_BLOCKWISE,  # noqa: F401
-                   ATTN_MASK_GLOBAL_SLIDING_WINDOW, ATTN_MASK_NONE, ATTN_MASK_PREFIX_LM,
-                   ATTN_MASK_SHARE_QUESTION, ATTN_MASK_SLIDING_WINDOW, ATTN_NORM_RELU,
-                   ATTN_NORM_SIGMOID, ATTN_NORM_SOFTMAX, AttnError, AttnVariantDesc, check, load,
-                   plan_tiles, row_range)
+from ._abi import (ATTN_BF16, ATTN_FLAG_VALIDATE, ATTN_FP32, ATTN_MASK_CAUSAL,  # noqa: F401
+                   ATTN_MASK_CAUSAL_BLOCKWISE, ATTN_MASK_GLOBAL_SLIDING_WINDOW, ATTN_MASK_NONE,
+                   ATTN_MASK_PREFIX_LM, ATTN_MASK_SHARE_QUESTION, ATTN_MASK_SLIDING_WINDOW,
+                   ATTN_MAX_SEGMENTS, ATTN_NORM_RELU, ATTN_NORM_SIGMOID, ATTN_NORM_SOFTMAX,
+                   AttnError, AttnVariantDesc, check, load, plan_tiles, row_range)
 
-__all__ = ["fwd", "make_desc", "AttnError", "AttnVariantDesc", "load", "plan_tiles", "row_range",
-           "ATTN_BF16", "ATTN_FP32", "ATTN_MASK_NONE", "ATTN_MASK_CAUSAL",
+__all__ = ["fwd", "make_desc", "lse_shape", "AttnError", "AttnVariantDesc", "load", "plan_tiles",
+           "row_range", "ATTN_BF16", "ATTN_FP32", "ATTN_MASK_NONE", "ATTN_MASK_CAUSAL",
            "ATTN_MASK_SLIDING_WINDOW", "ATTN_MASK_PREFIX_LM", "ATTN_MASK_GLOBAL_SLIDING_WINDOW",
            "ATTN_MASK_SHARE_QUESTION", "ATTN_MASK_CAUSAL_BLOCKWISE", "ATTN_NORM_SOFTMAX",
-           "ATTN_NORM_RELU", "ATTN_NORM_SIGMOID"]
+           "ATTN_NORM_RELU", "ATTN_NORM_SIGMOID", "ATTN_FLAG_VALIDATE"]
 
 _DTYPES = {torch.bfloat16: ATTN_BF16, torch.float32: ATTN_FP32}
 _MASKS = {"none": ATTN_MASK_NONE, "causal": ATTN_MASK_CAUSAL,
@@ -32,24 +36,71 @@ _MASKS = {"none": ATTN_MASK_NONE, "causal": ATTN_MASK_CAUSAL,
           "share_question": ATTN_MASK_SHARE_QUESTION,
           "causal_blockwise": ATTN_MASK_CAUSAL_BLOCKWISE}
 _NORMS = {"softmax": ATTN_NORM_SOFTMAX, "relu": ATTN_NORM_RELU, "sigmoid": ATTN_NORM_SIGMOID}
+_ORDERS = {None: 0, "natural": 1, "xcd_groups": 2}
+
+
+def _int_array(t, name, device):
+    if t.dtype != torch.int32 or t.device != device or not t.is_contiguous():
+        raise TypeError(f"{name} must be contiguous int32 on q's device")
+    if t.dim() != 1:
+        raise ValueError(f"{name} must be one-dimensional")
+
+
+def lse_shape(q, varlen: bool):
+    """Shape of the fp32 LSE output for q: (B, Hq, Sq), or (Hq, Tq) when varlen."""
+    return (q.shape[1], q.shape[0]) if varlen else (q.shape[0], q.shape[1], q.shape[2])
+
+
+def _check_shapes(q, k, v, out, varlen, alibi_slopes):
+    want = 3 if varlen else 4
+    layout = "[T, H, D]" if varlen else "[B, H, S, D]"
+    for name, t in (("q", q), ("k", k), ("v", v), ("out", out)):
+        if t.dim() != want:
+            raise ValueError(f"{name} must be {layout}, got shape {tuple(t.shape)}")
+        if t.device != q.device:
+            raise TypeError(f"{name} is on {t.device}, q on {q.device}")
+        if t.stride(-1) != 1:
+            raise ValueError("head_dim must be the innermost, contiguous axis")
+    if k.shape != v.shape:
+        raise ValueError(f"k {tuple(k.shape)} and v {tuple(v.shape)} differ")
+    if k.shape[-1] != q.shape[-1]:
+        raise ValueError(f"head_dim of k ({k.shape[-1]}) differs from q ({q.shape[-1]})")
+    if out.shape != q.shape:
+        raise ValueError(f"out {tuple(out.shape)} must have q's shape {tuple(q.shape)}")
+    if not varlen and k.shape[0] != q.shape[0]:
+        raise ValueError(f"batch of k/v ({k.shape[0]}) differs from q ({q.shape[0]})")
+    if alibi_slopes is not None:
+        if alibi_slopes.dtype != torch.float32 or alibi_slopes.device != q.device \
+                or not alibi_slopes.is_contiguous():
+            raise TypeError("alibi_slopes must be contiguous fp32 on q's device")
+        hq = q.shape[1]
+        if alibi_slopes.numel() != hq:
+            raise ValueError(f"alibi_slopes has {alibi_slopes.numel()} entries, q has {hq} heads")
 
 
 def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, softcap=0.0,
               scale=None, cu_seqlens_q=None, cu_seqlens_k=None, max_seqlen_q=None,
               max_seqlen_k=None, stream=None, mask=None, prefix_len=0, num_global=0,
-              segment_starts=None, query_start=0, relative_position=False,
-              norm="softmax") -> AttnVariantDesc:
+              global_tokens=None, segment_starts=None, query_start=0, relative_position=False,
+              norm="softmax", validate=False, heads_per_wg=0, order=None,
+              chunk=0) -> AttnVariantDesc:
     """Build the descriptor for tensors q/k/v/out (see include/attn.h for layouts).
 
     `mask` names any attn_mask_kind_t ("prefix_lm", "global_sliding_window",
     "share_question", "causal_blockwise", ...) and overrides causal/window;
-    `window` gives the (left, right) bounds of the two window masks.
+    `window` gives the (left, right) bounds of the two window masks;
+    `global_tokens` (device int32, strictly increasing) lists the global
+    positions of the global sliding window (else positions 0..num_global-1).
+    `validate` sets ATTN_FLAG_VALIDATE (host check of cu_seqlens, segments and
+    global positions). `heads_per_wg`, `order` ("natural", "xcd_groups") and
+    `chunk` override the library's workgroup schedule (tuning and tests).
     """
     if q.dtype not in _DTYPES or k.dtype != q.dtype or v.dtype != q.dtype or out.dtype != q.dtype:
         raise TypeError("q, k, v, out must share dtype bfloat16 or float32")
+    varlen = cu_seqlens_q is not None
+    _check_shapes(q, k, v, out, varlen, alibi_slopes)
     d = AttnVariantDesc.new()
     d.dtype = _DTYPES[q.dtype]
-    varlen = cu_seqlens_q is not None
     D = q.shape[-1]
     d.head_dim = D
     d.scale = float(scale) if scale is not None else 1.0 / math.sqrt(D)
@@ -67,22 +118,27 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
     d.relative_position = 1 if relative_position else 0
     d.norm_kind = _NORMS[norm] if isinstance(norm, str) else int(norm)
     if segment_starts is not None:
-        if (segment_starts.dtype != torch.int32 or segment_starts.device != q.device
-                or not segment_starts.is_contiguous()):
-            raise TypeError("segment_starts must be contiguous int32 on q's device")
+        _int_array(segment_starts, "segment_starts", q.device)
         d.segment_starts = segment_starts.data_ptr()
         d.num_segments = segment_starts.numel()
+    if global_tokens is not None:
+        _int_array(global_tokens, "global_tokens", q.device)
+        if num_global and int(num_global) != global_tokens.numel():
+            raise ValueError(f"num_global={num_global} but global_tokens has "
+                             f"{global_tokens.numel()} entries")
+        d.num_global = global_tokens.numel()
+        d.global_tokens = global_tokens.data_ptr() if global_tokens.numel() else None
     d.softcap = float(softcap)
     if alibi_slopes is not None:
-        if alibi_slopes.dtype != torch.float32 or alibi_slopes.device != q.device:
-            raise TypeError("alibi_slopes must be fp32 on q's device")
         d.alibi_slopes = alibi_slopes.data_ptr()
     if varlen:
         if cu_seqlens_k is None:
             cu_seqlens_k = cu_seqlens_q
-        for cu in (cu_seqlens_q, cu_seqlens_k):
-            if cu.dtype != torch.int32 or cu.device != q.device or not cu.is_contiguous():
-                raise TypeError("cu_seqlens must be contiguous int32 on q's device")
+        _int_array(cu_seqlens_q, "cu_seqlens_q", q.device)
+        _int_array(cu_seqlens_k, "cu_seqlens_k", q.device)
+        if cu_seqlens_k.numel() != cu_seqlens_q.numel() or cu_seqlens_q.numel() < 1:
+            raise ValueError(f"cu_seqlens_q ({cu_seqlens_q.numel()}) and cu_seqlens_k "
+                             f"({cu_seqlens_k.numel()}) must both hold batch + 1 >= 1 entries")
         if max_seqlen_q is None or max_seqlen_k is None:
             raise ValueError("varlen needs max_seqlen_q and max_seqlen_k (no device readback)")
         d.batch = cu_seqlens_q.numel() - 1
@@ -93,8 +149,6 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
         for name, t in (("q", q), ("k", k), ("v", v), ("o", out)):
             setattr(d, f"stride_{name}_h", t.stride(1))
             setattr(d, f"stride_{name}_s", t.stride(0))
-            if t.stride(2) != 1:
-                raise ValueError("head_dim must be the innermost, contiguous axis")
     else:
         d.batch, d.num_q_heads, d.seqlen_q = q.shape[0], q.shape[1], q.shape[2]
         d.num_kv_heads, d.seqlen_k = k.shape[1], k.shape[2]
@@ -102,8 +156,10 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
             setattr(d, f"stride_{name}_b", t.stride(0))
             setattr(d, f"stride_{name}_h", t.stride(1))
             setattr(d, f"stride_{name}_s", t.stride(2))
-            if t.stride(3) != 1:
-                raise ValueError("head_dim must be the innermost, contiguous axis")
+    d.flags = ATTN_FLAG_VALIDATE if validate else 0
+    d.sched_heads_per_wg = int(heads_per_wg)
+    d.sched_order = _ORDERS[order]
+    d.sched_chunk = int(chunk)
     if stream is None:
         stream = torch.cuda.current_stream(q.device).cuda_stream
     d.stream = stream
@@ -113,16 +169,18 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
 def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softcap: float = 0.0,
         scale: Optional[float] = None, cu_seqlens_q=None, cu_seqlens_k=None, max_seqlen_q=None,
         max_seqlen_k=None, out=None, lse=None, return_lse: bool = True, mask=None,
-        prefix_len: int = 0, num_global: int = 0, segment_starts=None, query_start: int = 0,
-        relative_position: bool = False, norm="softmax"):
+        prefix_len: int = 0, num_global: int = 0, global_tokens=None, segment_starts=None,
+        query_start: int = 0, relative_position: bool = False, norm="softmax",
+        validate: bool = False, heads_per_wg: int = 0, order=None, chunk: int = 0):
     """Attention forward on the GPU.
 
     Fixed length: q [B,Hq,S,D], k/v [B,Hkv,Sk,D] -> out like q, lse [B,Hq,S] fp32.
     Varlen: q [Tq,Hq,D], k/v [Tk,Hkv,D], cu_seqlens int32 [B+1] -> lse [Hq,Tq].
     window=(left, right) selects the sliding-window mask (-1 = unbounded).
     The other variants of include/attn.h are selected by `mask` (with
-    prefix_len, num_global, segment_starts, query_start), `relative_position`
-    and `norm` ("softmax", "relu", "sigmoid"; only softmax produces an LSE).
+    prefix_len, num_global / global_tokens, segment_starts, query_start),
+    `relative_position` and `norm` ("softmax", "relu", "sigmoid"; only softmax
+    produces an LSE). See make_desc for `validate` and the schedule overrides.
     """
     if not q.is_cuda:
         raise ValueError("fwd runs on the GPU only; q, k, v must be device tensors")
@@ -134,16 +192,20 @@ def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softca
     if not softmax:
         return_lse, lse = False, None
     if lse is None and return_lse:
-        shape = (q.shape[1], q.shape[0]) if varlen else (q.shape[0], q.shape[1], q.shape[2])
-        lse = torch.empty(shape, dtype=torch.float32, device=q.device)
-    if lse is not None and (lse.dtype != torch.float32 or not lse.is_contiguous()):
-        raise TypeError("lse must be contiguous fp32")
+        lse = torch.empty(lse_shape(q, varlen), dtype=torch.float32, device=q.device)
+    if lse is not None:
+        if lse.dtype != torch.float32 or not lse.is_contiguous() or lse.device != q.device:
+            raise TypeError("lse must be contiguous fp32 on q's device")
+        if tuple(lse.shape) != tuple(lse_shape(q, varlen)):
+            raise ValueError(f"lse {tuple(lse.shape)} must be {tuple(lse_shape(q, varlen))}")
     d = make_desc(q, k, v, out, causal=causal, window=window, alibi_slopes=alibi_slopes,
                   softcap=softcap, scale=scale, cu_seqlens_q=cu_seqlens_q,
                   cu_seqlens_k=cu_seqlens_k, max_seqlen_q=max_seqlen_q,
                   max_seqlen_k=max_seqlen_k, mask=mask, prefix_len=prefix_len,
-                  num_global=num_global, segment_starts=segment_starts, query_start=query_start,
-                  relative_position=relative_position, norm=norm)
+                  num_global=num_global, global_tokens=global_tokens,
+                  segment_starts=segment_starts, query_start=query_start,
+                  relative_position=relative_position, norm=norm, validate=validate,
+                  heads_per_wg=heads_per_wg, order=order, chunk=chunk)
     status = lib.attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                           lse.data_ptr() if lse is not None else None, ctypes.byref(d))
     check(status, lib)

@@ -12,8 +12,9 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libattn.so")
 
-ATTN_ABI_VERSION = 2
+ATTN_ABI_VERSION = 3
 ATTN_MAX_SEGMENTS = 2048
+ATTN_FLAG_VALIDATE = 1
 ATTN_BF16, ATTN_FP32 = 0, 1
 ATTN_MASK_NONE, ATTN_MASK_CAUSAL, ATTN_MASK_SLIDING_WINDOW = 0, 1, 2
 ATTN_MASK_PREFIX_LM, ATTN_MASK_GLOBAL_SLIDING_WINDOW = 3, 4
@@ -70,6 +71,11 @@ class AttnVariantDesc(ctypes.Structure):
         ("segment_starts", ctypes.c_void_p),
         ("num_segments", ctypes.c_int32),
         ("query_start", ctypes.c_int32),
+        ("global_tokens", ctypes.c_void_p),
+        ("flags", ctypes.c_uint32),
+        ("sched_heads_per_wg", ctypes.c_int32),
+        ("sched_order", ctypes.c_int32),
+        ("sched_chunk", ctypes.c_int32),
     ]
 
     @classmethod

@@ -1,12 +1,14 @@
 // attn_api.cpp -- C ABI of libattn.so: validation, planning and dispatch.
 //
 // Every check runs on the host before the first HIP call, so a rejected call
-// has no side effect and the error paths are testable without a GPU.
+// has no side effect and the error paths are testable without a GPU. Only
+// ATTN_FLAG_VALIDATE reads device memory (the cu_seqlens, segment and global
+// position arrays, copied to the host) before the launch.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 #include <cstdint>
-#include <cstdlib>
+#include <vector>
 
 #include "../../include/attn.h"
 #include "kernel_params.h"
@@ -50,6 +52,81 @@ bool slice_fits(int64_t rows, int64_t stride_s, int64_t d, int64_t elt_bytes, in
     if (rows <= 0) return true;
     int64_t bytes = ((rows + pad_rows) * stride_s + d) * elt_bytes;
     return bytes < (int64_t(1) << 31);
+}
+
+// Do the D-element rows of an output with these sizes and strides stay
+// disjoint? Ordered by stride, every dimension must step past the whole extent
+// of the ones inside it (sufficient, and what every ordinary layout meets);
+// dimensions of size one are ignored. Overlapping output rows would make the
+// result depend on which workgroup writes last.
+bool rows_disjoint(int64_t d, int n, const int64_t* size, const int64_t* stride)
+{
+    int64_t sz[3], st[3];
+    int m = 0;
+    for (int i = 0; i < n; ++i)
+        if (size[i] > 1) {
+            sz[m] = size[i];
+            st[m] = stride[i];
+            ++m;
+        }
+    for (int a = 0; a < m; ++a)  // insertion sort by stride
+        for (int b = a; b > 0 && st[b] < st[b - 1]; --b) {
+            int64_t t = st[b]; st[b] = st[b - 1]; st[b - 1] = t;
+            t = sz[b]; sz[b] = sz[b - 1]; sz[b - 1] = t;
+        }
+    int64_t extent = d;  // elements covered by one row
+    for (int a = 0; a < m; ++a) {
+        if (st[a] < extent) return false;
+        extent = st[a] * (sz[a] - 1) + extent;
+    }
+    return true;
+}
+
+// Host copy of a device int32 array, on `stream` (ATTN_FLAG_VALIDATE only).
+bool fetch_i32(const int32_t* dev, int64_t n, hipStream_t stream, std::vector<int32_t>* out)
+{
+    out->assign((size_t)n, 0);
+    if (n == 0) return true;
+    if (hipMemcpyAsync(out->data(), dev, (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost,
+                       stream) != hipSuccess)
+        return false;
+    return hipStreamSynchronize(stream) == hipSuccess;
+}
+
+bool strictly_increasing_nonneg(const std::vector<int32_t>& a)
+{
+    for (size_t i = 0; i < a.size(); ++i)
+        if (a[i] < 0 || (i > 0 && a[i] <= a[i - 1])) return false;
+    return true;
+}
+
+// ATTN_FLAG_VALIDATE: check the device-side preconditions on the host.
+int validate_device_inputs(const attn_variant_desc& d, bool varlen, bool segments, bool glist)
+{
+    hipStream_t stream = static_cast<hipStream_t>(d.stream);
+    std::vector<int32_t> a;
+    if (varlen) {
+        const int32_t* cus[2] = {d.cu_seqlens_q, d.cu_seqlens_k};
+        const int64_t total[2] = {d.total_q, d.total_k};
+        const int64_t maxlen[2] = {d.max_seqlen_q, d.max_seqlen_k};
+        for (int t = 0; t < 2; ++t) {
+            if (!fetch_i32(cus[t], (int64_t)d.batch + 1, stream, &a)) return ATTN_ERR_LAUNCH;
+            if (a[0] != 0 || a[(size_t)d.batch] != total[t]) return ATTN_ERR_BAD_SHAPE;
+            for (int32_t s = 0; s < d.batch; ++s) {
+                const int64_t len = (int64_t)a[(size_t)s + 1] - a[(size_t)s];
+                if (len < 0 || len > maxlen[t]) return ATTN_ERR_BAD_SHAPE;
+            }
+        }
+    }
+    if (segments) {
+        if (!fetch_i32(d.segment_starts, d.num_segments, stream, &a)) return ATTN_ERR_LAUNCH;
+        if (!strictly_increasing_nonneg(a)) return ATTN_ERR_BAD_VARIANT;
+    }
+    if (glist) {
+        if (!fetch_i32(d.global_tokens, d.num_global, stream, &a)) return ATTN_ERR_LAUNCH;
+        if (!strictly_increasing_nonneg(a)) return ATTN_ERR_BAD_VARIANT;
+    }
+    return ATTN_OK;
 }
 
 }  // namespace
@@ -122,6 +199,13 @@ static int check_variant(const attn_variant_desc* d)
     if (d->relative_position != 0 && d->relative_position != 1) return ATTN_ERR_BAD_VARIANT;
     if (!std::isfinite(d->scale) || !(d->scale > 0.0f)) return ATTN_ERR_BAD_VARIANT;
     if (!std::isfinite(d->softcap) || d->softcap < 0.0f) return ATTN_ERR_BAD_VARIANT;
+    // the kernels scale the dot product by 2 log2(e) scale / C: it must be finite
+    if (d->softcap > 0.0f && !std::isfinite(d->scale / d->softcap * (float)(2.0 * 1.4426950408889634)))
+        return ATTN_ERR_BAD_VARIANT;
+    if (d->mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d->global_tokens &&
+        d->num_global > ATTN_MAX_SEGMENTS)
+        return ATTN_ERR_BAD_VARIANT;
+    if (d->flags & ~ATTN_FLAG_VALIDATE) return ATTN_ERR_BAD_VARIANT;
     return ATTN_OK;
 }
 
@@ -215,10 +299,17 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     // which leaves fewer partially visible tiles at the mask edges.
     const int group = d.num_q_heads / d.num_kv_heads;
     int hp = d.dtype != ATTN_BF16 ? 1 : group % 4 == 0 ? 4 : group % 2 == 0 ? 2 : 1;
-    if (const char* env = std::getenv("ATTN_HEADS_PER_WG")) {  // experiments: 1, 2 or 4
-        const int h = std::atoi(env);
-        if (d.dtype == ATTN_BF16 && (h == 1 || h == 2 || h == 4) && group % h == 0) hp = h;
+    if (d.sched_heads_per_wg != 0) {  // tuning override: 1, 2 or 4 dividing the group
+        const int h = d.sched_heads_per_wg;
+        if ((h != 1 && h != 2 && h != 4) || group % h != 0 || (d.dtype != ATTN_BF16 && h != 1))
+            return ATTN_ERR_BAD_VARIANT;
+        hp = h;
     }
+    if (d.sched_order < 0 || d.sched_order > 2) return ATTN_ERR_BAD_VARIANT;
+    if (d.sched_order == 2 && ((int64_t)d.batch * d.num_kv_heads) % 8 != 0)
+        return ATTN_ERR_BAD_VARIANT;
+    if (d.sched_chunk < 0 || (d.sched_chunk > 0 && d.sched_order == 1))
+        return ATTN_ERR_BAD_VARIANT;
     const int block_m = d.dtype == ATTN_BF16 ? attn::bf16_block_m() / hp : attn::f32_block_m();
     // a multiple of hp: the hp query tiles of one 128-row span are issued
     // together (their K/V reads then meet in the L2)
@@ -229,6 +320,13 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
 
     if (!q || !k || !v || !out) return ATTN_ERR_NULL_PTR;
     if (segment_mask(d.mask_kind) && !d.segment_starts) return ATTN_ERR_NULL_PTR;
+    {
+        // output rows must not overlap (inputs may: a broadcast K/V is fine)
+        const int64_t osize[3] = {varlen ? d.total_q : (int64_t)d.batch, d.num_q_heads,
+                                  varlen ? 1 : max_q};
+        const int64_t ostride[3] = {varlen ? p.so_s : p.so_b, p.so_h, p.so_s};
+        if (!rows_disjoint(D, 3, osize, ostride)) return ATTN_ERR_BAD_SHAPE;
+    }
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
         return ATTN_ERR_ALIGNMENT;
     if ((reinterpret_cast<uintptr_t>(lse) & 3u) != 0) return ATTN_ERR_ALIGNMENT;
@@ -283,6 +381,8 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     // would start only with their chunk and end after everything else
     // (measured unchunked at 268 MB of K/V: 1.25x and 1.03x faster).
     p.map_mode = ((int64_t)d.batch * d.num_kv_heads) % 8 == 0 ? 1 : 0;
+    if (d.sched_order != 0) p.map_mode = d.sched_order == 2 ? 1 : 0;
+    if (d.sched_chunk > 0 && p.map_mode != 1) return ATTN_ERR_BAD_VARIANT;
     {
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
         const int64_t kv_tokens = varlen ? d.total_k : (int64_t)d.batch * d.seqlen_k;
@@ -295,14 +395,10 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         if (chunk > groups_per_xcd) chunk = groups_per_xcd;
         p.chunk = (int32_t)(chunk > 0 ? chunk : 1);
     }
-    if (const char* env = std::getenv("ATTN_MAP_MODE")) {
-        int m = std::atoi(env);
-        if (m == 0 || (m == 1 && p.map_mode == 1)) p.map_mode = m;
-    }
-    if (const char* env = std::getenv("ATTN_CHUNK")) {  // kv groups per chunk (experiments)
-        int c = std::atoi(env);
+    if (d.sched_chunk > 0) {  // tuning override: kv groups per chunk
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
-        if (c >= 1 && c <= groups_per_xcd) p.chunk = c;
+        if (d.sched_chunk > groups_per_xcd) return ATTN_ERR_BAD_VARIANT;
+        p.chunk = d.sched_chunk;
     }
     // Divisors of the workgroup-id decode (all >= 1; blocks <= INT32_MAX
     // bounds every dividend).
@@ -321,6 +417,13 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         p.div_chunk_full = make_fastdiv((uint32_t)(p.chunk * gsets));
         p.div_chunk_last = make_fastdiv((uint32_t)(last_groups * gsets));
         p.last_chunk = (int32_t)last;
+    }
+    const bool glist = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.global_tokens &&
+                       d.num_global > 0;
+    if (glist) return ATTN_ERR_UNSUPPORTED;
+    if (d.flags & ATTN_FLAG_VALIDATE) {
+        rc = validate_device_inputs(d, varlen, segment_mask(d.mask_kind), glist);
+        if (rc != ATTN_OK) return rc;
     }
     hipStream_t stream = static_cast<hipStream_t>(d.stream);
     hipError_t err = d.dtype == ATTN_BF16 ? attn::launch_bf16(p, d.head_dim, stream)

@@ -1101,14 +1101,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
 // Keys per tile. 64 halves the per-tile barrier, load-wait and max-exchange
 // overhead relative to 32 and still fits the pipeline's double-buffered
 // scores in the registers of two waves per SIMD.
-constexpr int key_tile_width(int)
-{
-#ifdef ATTN_BN
-    return ATTN_BN;
-#else
-    return 64;
-#endif
-}
+constexpr int key_tile_width(int) { return 64; }
 
 template <int D, int CAP, int BIAS, int NORM, bool GEN, bool LEFT = true>
 hipError_t launch_variant(const AttnParams& p, hipStream_t stream)

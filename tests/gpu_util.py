@@ -30,14 +30,15 @@ def log(msg: str) -> None:
     sys.stdout.flush()
 
 
-def run_gpu(inp: Inputs, *, out=None, lse=None, q=None, k=None, v=None):
-    """Run the library on `inp` (tensors moved to cuda:0 unless given). Returns
+def run_gpu(inp: Inputs, *, out=None, lse=None, q=None, k=None, v=None, **extra):
+    """Run the library on `inp` (tensors moved to cuda:0 unless given); `extra`
+    passes further fwd arguments (schedule overrides, validate). Returns
     (out, lse); lse is None for the ReLU / Sigmoid normalisations."""
     dev = torch.device("cuda:0")
     q = inp.q.to(dev) if q is None else q
     k = inp.k.to(dev) if k is None else k
     v = inp.v.to(dev) if v is None else v
-    res = attn.fwd(q, k, v, out=out, lse=lse, **inp.variant_kwargs(dev))
+    res = attn.fwd(q, k, v, out=out, lse=lse, **inp.variant_kwargs(dev), **extra)
     return res if isinstance(res, tuple) else (res, None)
 
 

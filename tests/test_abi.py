@@ -141,6 +141,35 @@ CASES = [
      "ATTN_ERR_BAD_VARIANT"),
     ("segments missing", lambda d: (setattr(d, "mask_kind", 5), setattr(d, "num_segments", 3)),
      "ATTN_ERR_NULL_PTR"),
+    # 2 log2(e) scale / C overflows fp32 for a tiny cap
+    ("softcap too small", lambda d: setattr(d, "softcap", 1e-40), "ATTN_ERR_BAD_VARIANT"),
+    ("too many global positions", lambda d: (setattr(d, "mask_kind", 4), setattr(d, "global_tokens", P),
+                                             setattr(d, "num_global", _abi.ATTN_MAX_SEGMENTS + 1)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("unknown flag", lambda d: setattr(d, "flags", 2), "ATTN_ERR_BAD_VARIANT"),
+    ("heads per wg 3", lambda d: setattr(d, "sched_heads_per_wg", 3), "ATTN_ERR_BAD_VARIANT"),
+    ("heads per wg 8", lambda d: setattr(d, "sched_heads_per_wg", 8), "ATTN_ERR_BAD_VARIANT"),
+    ("heads per wg not dividing", lambda d: (setattr(d, "num_q_heads", 6), setattr(d, "num_kv_heads", 3),
+                                             setattr(d, "sched_heads_per_wg", 4)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("heads per wg fp32", lambda d: (setattr(d, "dtype", _abi.ATTN_FP32), setattr(d, "sched_heads_per_wg", 2)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("order 3", lambda d: setattr(d, "sched_order", 3), "ATTN_ERR_BAD_VARIANT"),
+    ("xcd order needs B*Hkv % 8", lambda d: setattr(d, "sched_order", 2), "ATTN_ERR_BAD_VARIANT"),
+    ("chunk with natural order", lambda d: (setattr(d, "sched_order", 1), setattr(d, "sched_chunk", 1)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("chunk without xcd order", lambda d: setattr(d, "sched_chunk", 1), "ATTN_ERR_BAD_VARIANT"),
+    ("chunk beyond groups", lambda d: (setattr(d, "batch", 4), setattr(d, "sched_chunk", 2)),
+     "ATTN_ERR_BAD_VARIANT"),
+    ("negative chunk", lambda d: setattr(d, "sched_chunk", -1), "ATTN_ERR_BAD_VARIANT"),
+    # output rows must be disjoint: heads on top of each other, or rows that
+    # overlap the next head
+    ("out heads overlap", lambda d: setattr(d, "stride_o_h", 128), "ATTN_ERR_BAD_SHAPE"),
+    ("out head stride below D", lambda d: setattr(d, "stride_o_h", 64), "ATTN_ERR_BAD_SHAPE"),
+    ("out rows run into the next head", lambda d: setattr(d, "stride_o_h", 99 * 128),
+     "ATTN_ERR_BAD_SHAPE"),
+    ("out batches overlap", lambda d: setattr(d, "stride_o_b", 8 * 100 * 128 - 8),
+     "ATTN_ERR_BAD_SHAPE"),
 ]
 
 
@@ -153,6 +182,9 @@ def test_validation_errors(lib, name, mutate, expect):
 
 VARLEN_CASES = [
     ("cu_k missing", lambda d: setattr(d, "cu_seqlens_k", None), "ATTN_ERR_NULL_PTR"),
+    ("out token stride below the heads", lambda d: setattr(d, "stride_o_s", 4 * 128),
+     "ATTN_ERR_BAD_SHAPE"),
+    ("out head stride below D", lambda d: setattr(d, "stride_o_h", 64), "ATTN_ERR_BAD_SHAPE"),
     ("max_seqlen < 0", lambda d: setattr(d, "max_seqlen_q", -1), "ATTN_ERR_BAD_SHAPE"),
     ("total < 0", lambda d: setattr(d, "total_k", -1), "ATTN_ERR_BAD_SHAPE"),
     ("total beyond int32", lambda d: setattr(d, "total_q", 1 << 33), "ATTN_ERR_UNSUPPORTED"),
@@ -196,3 +228,24 @@ def test_empty_problems_do_nothing(lib):
     d = base_desc(varlen=True)
     d.max_seqlen_q = 0
     assert call(lib, d, q=None, k=None, v=None, o=None, lse=None) == 0
+
+
+def test_disjoint_strided_outputs_accepted(lib):
+    """Interleaved but disjoint output layouts pass the overlap check."""
+    for mut in (lambda d: (setattr(d, "stride_o_s", 8 * 128), setattr(d, "stride_o_h", 128),
+                           setattr(d, "stride_o_b", 100 * 8 * 128)),   # [B, S, H, D]
+                lambda d: (setattr(d, "stride_o_s", 136), setattr(d, "stride_o_h", 100 * 136),
+                           setattr(d, "stride_o_b", 8 * 100 * 136))):  # padded rows
+        d = base_desc()
+        mut(d)
+        # the overlap check passes, so the call reaches the pointer check (a
+        # rejected layout would return ATTN_ERR_BAD_SHAPE before it)
+        assert call(lib, d, q=None) == err("ATTN_ERR_NULL_PTR")
+
+
+def test_broadcast_inputs_accepted(lib):
+    """Inputs may overlap (a K/V head broadcast with stride 0 is read only)."""
+    d = base_desc()
+    d.stride_k_h = 0
+    d.stride_v_h = 0
+    assert call(lib, d, q=None) == err("ATTN_ERR_NULL_PTR")
