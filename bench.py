@@ -116,7 +116,7 @@ def read_traffic(workload: str):
         return None
     text = open(path).read()
     m_hash = re.search(r"kernel_hash:\s*([0-9a-f]+)", text)
-    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    m_bytes = re.search(r"fabric_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not m_hash or not m_bytes or m_hash.group(1) != kernel_hash():
         return None
     return float(m_bytes.group(1))

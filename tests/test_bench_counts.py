@@ -59,12 +59,12 @@ def _field(text, key):
 
 @pytest.mark.parametrize("name", TRAFFIC)
 def test_traffic_summary(name):
-    """Each committed HBM-traffic summary names a workload, states no fewer
+    """Each committed memory-traffic summary names a workload, states no fewer
     bytes than the method must move, and is used by bench.py only while its
-    kernel-source hash is the current one."""
+    library-source hash is the current one."""
     assert name in WORKLOADS
     text = open(os.path.join(bench.PROFILES, f"traffic_{name}.md")).read()
-    hbm = float(_field(text, "hbm_bytes_per_launch"))
+    hbm = float(_field(text, "fabric_bytes_per_launch"))
     alg = int(_field(text, "algorithmic_bytes_per_launch"))
     assert hbm >= 0.9 * alg
     if name == "causal_bf16":
