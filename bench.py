@@ -66,10 +66,15 @@ def row_counts(inp, S: int) -> np.ndarray:
         return np.maximum(0, hi - lo + 1)
     if wl.mask == MASK_PREFIX_LM:  # keys j < L_p, or j <= i
         return np.maximum(i + 1, min(wl.prefix_len, S))
-    if wl.mask == MASK_GLOBAL_WINDOW:  # |i - j| within the window, or i or j in 0..G-1
-        g = min(wl.num_global, S)
+    if wl.mask == MASK_GLOBAL_WINDOW:  # |i - j| within the window, or i or j in G
         lo, hi = band(wl.window_left, wl.window_right)
         inside = np.maximum(0, hi - lo + 1)
+        if wl.global_list:  # listed G: the keys of G outside the row's band
+            g = np.asarray([x for x in wl.global_list if x < S], dtype=np.int64)
+            in_band = ((g[None, :] >= lo[:, None]) & (g[None, :] <= hi[:, None])).sum(1)
+            n = inside + len(g) - in_band
+            return np.where(np.isin(i, g), S, n)
+        g = min(wl.num_global, S)
         overlap = np.maximum(0, np.minimum(hi, g - 1) - lo + 1)  # globals already in the band
         n = inside + g - overlap
         return np.where(i < g, S, n)
@@ -317,6 +322,7 @@ def main():
             "norm": wl.norm,
             "prefix_len": wl.prefix_len if wl.mask in (MASK_PREFIX_LM, MASK_SHARE_QUESTION) else None,
             "num_global": wl.num_global if wl.mask == MASK_GLOBAL_WINDOW else None,
+            "global_list": list(wl.global_list) if wl.global_list else None,
             "segment_starts": inp.segment_starts.tolist() if inp.segment_starts is not None else None,
             "query_start": wl.query_start if wl.mask == MASK_CAUSAL_BLOCKWISE else None,
             "unmasked_flops_per_step": flops,

@@ -251,7 +251,9 @@ int attn_plan_tiles(const attn_variant_desc *desc, int32_t q0, int32_t rows, int
  * out[1] <= j <= out[2] (empty when out[1] > out[2]). segment_starts is a
  * HOST copy of desc->segment_starts (read only for SHARE_QUESTION and
  * CAUSAL_BLOCKWISE); desc->segment_starts itself is not read. Reads the mask
- * fields of desc only.
+ * fields of desc only. A GLOBAL_SLIDING_WINDOW with a listed global set
+ * (global_tokens != NULL) is not of this form and returns
+ * ATTN_ERR_UNSUPPORTED.
  */
 int attn_row_range(const attn_variant_desc *desc, const int32_t *segment_starts, int32_t i,
                    int32_t lq, int32_t lk, int32_t out[3]);

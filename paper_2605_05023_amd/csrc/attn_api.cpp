@@ -131,6 +131,8 @@ int validate_device_inputs(const attn_variant_desc& d, bool varlen, bool segment
 
 }  // namespace
 
+static_assert(ATTN_MAX_SEGMENTS == kMaxGlobalList, "LDS staging of the listed global set");
+
 extern "C" int attn_abi_version(void) { return ATTN_ABI_VERSION; }
 
 extern "C" const char* attn_status_string(int status)
@@ -234,6 +236,10 @@ extern "C" int attn_row_range(const attn_variant_desc* desc, const int32_t* segm
     int rc = check_variant(desc);
     if (rc != ATTN_OK) return rc;
     if (segment_mask(desc->mask_kind) && !segment_starts) return ATTN_ERR_NULL_PTR;
+    // a listed global set is not a prefix plus a band
+    if (desc->mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && desc->global_tokens &&
+        desc->num_global > 0)
+        return ATTN_ERR_UNSUPPORTED;
     if (i < 0 || i >= lq || lk < 0) return ATTN_ERR_BAD_SHAPE;
     const int32_t* seg = segment_mask(desc->mask_kind) ? segment_starts : nullptr;
     const int32_t nseg = seg ? desc->num_segments : 0;
@@ -420,7 +426,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     }
     const bool glist = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.global_tokens &&
                        d.num_global > 0;
-    if (glist) return ATTN_ERR_UNSUPPORTED;
+    p.gtok = glist ? d.global_tokens : nullptr;
     if (d.flags & ATTN_FLAG_VALIDATE) {
         rc = validate_device_inputs(d, varlen, segment_mask(d.mask_kind), glist);
         if (rc != ATTN_OK) return rc;

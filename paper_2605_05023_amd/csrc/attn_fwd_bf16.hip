@@ -36,6 +36,11 @@ hipError_t launch_bf16(const AttnParams& p, int head_dim, hipStream_t stream)
 {
     const bool closed = p.mask_kind >= 0 && p.mask_kind <= 3;  // band masks of plan.h
     const bool both_biases = p.slopes != nullptr && p.relpos != 0;
+    if (p.gtok) {  // global sliding window with a listed global set
+        if (p.norm == kNormRelu) return launch_bf16_glist_relu(p, head_dim, stream);
+        if (p.norm == kNormSigmoid) return launch_bf16_glist_sigmoid(p, head_dim, stream);
+        return launch_bf16_glist_softmax(p, head_dim, stream);
+    }
     if (p.norm == kNormRelu) return launch_bf16_general_relu(p, head_dim, stream);
     if (p.norm == kNormSigmoid) return launch_bf16_general_sigmoid(p, head_dim, stream);
     if (!closed || both_biases) return launch_bf16_general_softmax(p, head_dim, stream);

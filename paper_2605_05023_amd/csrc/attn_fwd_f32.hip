@@ -107,8 +107,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     int t_lo, t_hi;  // key tiles visited
     if constexpr (GEN) {
         if (qi < lq)
-            rv = row_visibility(p.mask_kind, p.band, p.num_global, p.seg, p.num_seg,
-                                p.query_start, qi, lq, lk);
+            rv = p.gtok ? row_vis_listed(p.band, p.gtok, p.num_global, qi, lq, lk)
+                        : row_visibility(p.mask_kind, p.band, p.num_global, p.seg, p.num_seg,
+                                         p.query_start, qi, lq, lk);
         const bool any = rv.pfx > 0 || rv.jlo <= rv.jhi;
         const int first = any ? (rv.pfx > 0 ? 0 : rv.jlo) : 0x3fffffff;
         const int last = any ? (rv.jlo <= rv.jhi ? rv.jhi : rv.pfx - 1) : -1;
@@ -123,7 +124,12 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     }
     const int ip = qi + (lk - lq);
     // relative-position reference (see score_u): first visible key for softmax
-    const int jref = SOFTMAX ? (rv.pfx > 0 ? 0 : rv.jlo) : ip;
+    int jref = SOFTMAX ? (rv.pfx > 0 ? 0 : rv.jlo) : ip;
+    if (GEN && SOFTMAX && p.gtok) {  // the smallest visible key may be one of G
+        int jr = rv.jlo <= rv.jhi ? rv.jlo : 0x7fffffff;
+        if (p.num_global > 0 && p.gtok[0] < lk) jr = min(jr, p.gtok[0]);
+        jref = jr == 0x7fffffff ? 0 : jr;
+    }
     float bias_abs = 0.0f, bias_lin = 0.0f;
     if constexpr (BIAS == kBiasAlibi || BIAS == kBiasGeneral)
         if (p.slopes) bias_abs = -p.slopes[hq] * p.unit;
@@ -139,25 +145,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     // own LDS writes and reads needs a fence, not a workgroup barrier.
     float (*ks)[D] = reinterpret_cast<float (*)[D]>(lds + wave * 2 * BN * D * 4);
     float (*vs)[D] = reinterpret_cast<float (*)[D]>(lds + (wave * 2 + 1) * BN * D * 4);
-    for (int kt = t_lo + wave; kt < t_hi; kt += NW) {
-        const int j0 = kt * BN;
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // previous tile fully read
-#pragma unroll
-        for (int i = 0; i < BN * D / 4 / 64; ++i) {
-            int e = i * 64 + lane;
-            int r = e / (D / 4), c = e % (D / 4);
-            f32x4 kx = {0.f, 0.f, 0.f, 0.f}, vx = {0.f, 0.f, 0.f, 0.f};
-            if (j0 + r < lk) {
-                kx = *reinterpret_cast<const f32x4*>(kb + koff + (int64_t)(j0 + r) * p.sk_s + 4 * c);
-                vx = *reinterpret_cast<const f32x4*>(vb + voff + (int64_t)(j0 + r) * p.sv_s + 4 * c);
-            }
-            *reinterpret_cast<f32x4*>(&ks[r][4 * c]) = kx;
-            *reinterpret_cast<f32x4*>(&vs[r][4 * c]) = vx;
-        }
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // tile written
-        const bool band_hit = rv.jlo <= rv.jhi && rv.jhi >= j0 && rv.jlo <= j0 + BN - 1;
-        if (!band_hit && j0 >= rv.pfx) continue;  // row sees none of the tile
-        const bool full = j0 + BN <= rv.pfx || (rv.jlo <= j0 && j0 + BN - 1 <= rv.jhi);
+    // Scores, mask, online softmax and P V for the BN keys in ks / vs; key t
+    // of the tile sits at position jpos(t) and is visible iff vis(t).
+    auto consume = [&](auto jpos, auto vis) __attribute__((always_inline)) {
         float s[BN];
 #pragma unroll
         for (int j = 0; j < BN; ++j) s[j] = 0.0f;
@@ -177,9 +167,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
 #pragma unroll
         for (int j = 0; j < BN; ++j) {
             float x = MODS ? score_u<SOFTCAP, BIAS>(s[j], p.scale_u, p.softcap_pre, p.softcap_post_u,
-                                                    bias_abs, bias_lin, ip, jref, j0 + j)
+                                                    bias_abs, bias_lin, ip, jref, jpos(j))
                            : s[j] * p.scale_u;
-            if (!full && !row_sees(rv, j0 + j)) x = -__builtin_inff();
+            if (!vis(j)) x = -__builtin_inff();
             s[j] = x;
             mx = __builtin_fmaxf(mx, x);
         }
@@ -209,6 +199,46 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
                 o[4 * c + 2] = __builtin_fmaf(pe, vx[2], o[4 * c + 2]);
                 o[4 * c + 3] = __builtin_fmaf(pe, vx[3], o[4 * c + 3]);
             }
+        }
+    };
+    // K and V rows at positions key(r) (r < BN) into this wave's tiles; rows at
+    // or past the sequence end are zero.
+    auto stage = [&](auto key) __attribute__((always_inline)) {
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // previous tile fully read
+#pragma unroll
+        for (int i = 0; i < BN * D / 4 / 64; ++i) {
+            int e = i * 64 + lane;
+            int r = e / (D / 4), c = e % (D / 4);
+            const int j = key(r);
+            f32x4 kx = {0.f, 0.f, 0.f, 0.f}, vx = {0.f, 0.f, 0.f, 0.f};
+            if (j < lk) {
+                kx = *reinterpret_cast<const f32x4*>(kb + koff + (int64_t)j * p.sk_s + 4 * c);
+                vx = *reinterpret_cast<const f32x4*>(vb + voff + (int64_t)j * p.sv_s + 4 * c);
+            }
+            *reinterpret_cast<f32x4*>(&ks[r][4 * c]) = kx;
+            *reinterpret_cast<f32x4*>(&vs[r][4 * c]) = vx;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // tile written
+    };
+    for (int kt = t_lo + wave; kt < t_hi; kt += NW) {
+        const int j0 = kt * BN;
+        stage([&](int r) { return j0 + r; });
+        const bool band_hit = rv.jlo <= rv.jhi && rv.jhi >= j0 && rv.jlo <= j0 + BN - 1;
+        if (!band_hit && j0 >= rv.pfx) continue;  // row sees none of the tile
+        const bool full = j0 + BN <= rv.pfx || (rv.jlo <= j0 && j0 + BN - 1 <= rv.jhi);
+        consume([&](int j) { return j0 + j; }, [&](int j) { return full || row_sees(rv, j0 + j); });
+    }
+    // A listed global set (global sliding window): its keys outside the row's
+    // band, BN list entries per tile, the waves taking turns.
+    if (GEN && p.gtok) {
+        const int ng = p.num_global;
+        for (int g0 = wave * BN; g0 < ng; g0 += NW * BN) {
+            auto key = [&](int r) { return g0 + r < ng ? min(p.gtok[g0 + r], lk) : lk; };
+            stage(key);
+            consume(key, [&](int j) {
+                const int kj = key(j);
+                return qi < lq && kj < lk && !(kj >= rv.jlo && kj <= rv.jhi);
+            });
         }
     }
 

@@ -89,9 +89,15 @@ constexpr float PSUM_BOUND = 256.0f;
 // band has a left bound (otherwise every row's first visible key is 0 and
 // partial tiles only check the right bound, which also masks keys past the
 // sequence end).
-template <int D_, int BN_, int CAP_, int BIAS_, int NORM_, bool GEN_, bool LEFT_ = true>
+// GLIST: the global sliding window's global set is a listed set of positions
+// (general path only); its keys outside a row's band are visited after the
+// planned tiles as gathered tiles.
+template <int D_, int BN_, int CAP_, int BIAS_, int NORM_, bool GEN_, bool LEFT_ = true,
+          bool GLIST_ = false>
 struct Traits {
     static constexpr int D = D_, BN = BN_;
+    static constexpr bool GLIST = GLIST_;
+    static_assert(!GLIST_ || GEN_, "a listed global set takes the general path");
     static constexpr int CAP = CAP_;
     static constexpr bool SOFTCAP = CAP_ != kCapOff, MODS = SOFTCAP || BIAS_ != kBiasNone;
     static constexpr int BIAS = BIAS_, NORM = NORM_;
@@ -701,6 +707,75 @@ __device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, f
     pv_tile<T>(vread, pw, ws);
 }
 
+// Keys of a listed global set G that a row does not already see through its
+// band (Appendix A, Global Sliding Window: j in G is visible from every row),
+// visited after the planned tiles, BN list entries at a time. `gl` holds G in
+// LDS, sorted and padded with lk (past the sequence end) to a multiple of BN.
+// The K and V rows of such a gathered tile are fetched one by one (each lane's
+// direct loads take the row of its list entry) into the first K/V buffers in
+// the usual swizzled layout, and every element is masked and modified with its
+// own key position; the online softmax state simply continues.
+template <class T>
+__device__ void gathered_tiles(WaveState<T>& ws, const AttnParams& p, const int* gl, int ng,
+                               char* lds_k, char* lds_v, __amdgpu_buffer_rsrc_t krs,
+                               __amdgpu_buffer_rsrc_t vrs, uint32_t krow, uint32_t vrow, int lk,
+                               bool row_valid, int wave, int lane)
+{
+    // tile row and swizzled 16-byte chunk this lane loads in load 0 (load q
+    // covers the rows q * ROWS_PER_LOAD further, whose swizzle is the same)
+    const int pos0 = wave * 1024 + 16 * lane;
+    const int r0 = pos0 / T::ROWB;
+    const uint32_t chunk = (uint32_t)((((pos0 % T::ROWB) / 16) ^ chunk_swizzle<T::D>(r0)) * 16);
+    for (int g0 = 0; g0 < ng; g0 += T::BN) {
+        __syncthreads();  // every wave is done with the buffers
+#pragma unroll
+        for (int q = 0; q < T::LOADS; ++q) {
+            // rows past the sequence end (padding, or positions >= lk) read as zero
+            const int key = min(gl[g0 + r0 + q * T::ROWS_PER_LOAD], lk);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                krs, (lds_void*)(lds_k + (4 * q + wave) * 1024), 16, chunk + (uint32_t)key * krow, 0,
+                0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                vrs, (lds_void*)(lds_v + (4 * q + wave) * 1024), 16, chunk + (uint32_t)key * vrow, 0,
+                0, 0);
+        }
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+        __syncthreads();
+        qk_tile<T>(lds_k, ws, ws.sa);
+        float mx = -__builtin_inff();
+#pragma unroll
+        for (int b = 0; b < T::NB; ++b) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                // element (b, e) is list entry g0 + 8 lh + c
+                const int c = 32 * b + e + (e >= 8 ? 8 : 0);
+                const int j = gl[g0 + 8 * ws.lh + c];
+                float x = ws.sa[b][e];
+                if constexpr (T::MODS)
+                    x = score_tile_u<T::CAP, T::BIAS>(
+                        x, p.scale_u, T::CAP == kCapShort ? p.softcap_pre2 : p.softcap_pre,
+                        p.softcap_post_u, ws.bias_abs, ws.bias_lin, (float)(ws.ip - j),
+                        (float)(ws.jref - j));
+                const bool vis = row_valid && j < lk && !(j >= ws.jlo && j <= ws.jhi);
+                x = vis ? x : -__builtin_inff();
+                ws.sa[b][e] = x;
+                mx = __builtin_fmaxf(mx, x);
+            }
+        }
+        if constexpr (T::SOFTMAX) {
+            mx = pair_max(mx);
+            if constexpr (!T::MODS) mx *= p.scale_u;  // raw max -> units (scale > 0)
+            update_max(ws, mx);
+            rescale_if_needed(ws);
+        }
+        const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
+        u32x4 pw[T::NB][2];
+        const RowSums rs = exp_tile<T>(ws.sa, pw, m_use, p.scale_u);
+        check_tile<T>(ws, ws.sa, pw, rs, p, 0);
+        pv_tile<T>(lds_v, pw, ws);
+    }
+}
+
 __device__ __forceinline__ int wave_min(int x)
 {
 #pragma unroll
@@ -892,6 +967,9 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     TileRanges tr = {};
     int jbeg, jend;
     TilePlan gp = {};
+    // listed global set: G in LDS, padded with lk to a multiple of BN
+    __shared__ __attribute__((aligned(16))) int gl[T::GLIST ? kMaxGlobalList + BN : 4];
+    int ng = 0;
     if constexpr (T::GEN) {
         __shared__ int red[4][8];
         const int32_t* seg = p.seg;
@@ -901,10 +979,20 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             __syncthreads();
             seg = sl;
         }
+        if constexpr (T::GLIST) {
+            ng = p.num_global;
+            const int npad = (ng + BN - 1) / BN * BN;
+            for (int i = tid; i < npad; i += NT) gl[i] = i < ng ? p.gtok[i] : lk;
+            __syncthreads();
+        }
         RowVis rv = {0, 1, 0};
-        if (qi < lq)
-            rv = row_visibility(p.mask_kind, p.band, p.num_global, seg, p.num_seg, p.query_start,
-                                qi, lq, lk);
+        if (qi < lq) {
+            if constexpr (T::GLIST)
+                rv = row_vis_listed(p.band, gl, ng, qi, lq, lk);
+            else
+                rv = row_visibility(p.mask_kind, p.band, p.num_global, seg, p.num_seg,
+                                    p.query_start, qi, lq, lk);
+        }
         ws.pfx = rv.pfx;
         ws.jlo = rv.jlo;
         ws.jhi = rv.jhi;
@@ -920,6 +1008,11 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     // Relative-position reference: the row's first visible key for softmax
     // (largest bias; the shift is added back to the LSE), i' otherwise.
     ws.jref = T::SOFTMAX ? (ws.pfx > 0 ? 0 : ws.jlo) : ws.ip;
+    if constexpr (T::GLIST && T::SOFTMAX) {  // the smallest visible key may be one of G
+        int jr = ws.jlo <= ws.jhi ? ws.jlo : 0x7fffffff;
+        if (ng > 0 && gl[0] < lk) jr = min(jr, gl[0]);
+        ws.jref = jr == 0x7fffffff ? 0 : jr;
+    }
     ws.bias_abs = 0.0f;
     ws.bias_lin = 0.0f;
     if constexpr (T::BIAS == kBiasAlibi) ws.bias_abs = -p.slopes[hq] * p.unit;
@@ -1056,6 +1149,9 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         else
             last_step<T>(lds_v0, ws, ws.sa, p, m_use, tile_of(j) * BN);
     }
+    if constexpr (T::GLIST)
+        gathered_tiles<T>(ws, p, gl, ng, lds_k0, lds_v0, krs, vrs, krow, vrow, lk, qi < lq, wave,
+                          lane);
 
     // Epilogue. Softmax: O = O^T / l (with PSUM_BF16 the sum of the bf16 P
     // O was made from), LSE = (m + log2 l) ln 2 with the fp32 l (+ the relative
@@ -1103,10 +1199,10 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
 // scores in the registers of two waves per SIMD.
 constexpr int key_tile_width(int) { return 64; }
 
-template <int D, int CAP, int BIAS, int NORM, bool GEN, bool LEFT = true>
+template <int D, int CAP, int BIAS, int NORM, bool GEN, bool LEFT = true, bool GLIST = false>
 hipError_t launch_variant(const AttnParams& p, hipStream_t stream)
 {
-    using T = Traits<D, key_tile_width(D), CAP, BIAS, NORM, GEN, LEFT>;
+    using T = Traits<D, key_tile_width(D), CAP, BIAS, NORM, GEN, LEFT, GLIST>;
     int64_t blocks = (int64_t)p.num_q_tiles * (p.hq >> p.hp_shift) * p.batch;
     hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)blocks), dim3(NT), 0, stream, p);
     return hipGetLastError();
@@ -1123,18 +1219,19 @@ hipError_t with_cap(const AttnParams& p, F&& f)
 }
 
 // The general-path instantiations of one normalisation: head dim, soft-cap,
-// and a runtime-coefficient bias when ALiBi or the relative position is on.
-template <int NORM>
+// and a runtime-coefficient bias when ALiBi or the relative position is on;
+// GLIST for a listed global set.
+template <int NORM, bool GLIST = false>
 hipError_t launch_general_norm(const AttnParams& p, int head_dim, hipStream_t stream)
 {
     const bool bias = p.slopes != nullptr || p.relpos != 0;
     return with_cap(p, [&](auto cap) {
         constexpr int C = decltype(cap)::value;
         if (head_dim == 128)
-            return bias ? launch_variant<128, C, kBiasGeneral, NORM, true>(p, stream)
-                        : launch_variant<128, C, kBiasNone, NORM, true>(p, stream);
-        return bias ? launch_variant<64, C, kBiasGeneral, NORM, true>(p, stream)
-                    : launch_variant<64, C, kBiasNone, NORM, true>(p, stream);
+            return bias ? launch_variant<128, C, kBiasGeneral, NORM, true, true, GLIST>(p, stream)
+                        : launch_variant<128, C, kBiasNone, NORM, true, true, GLIST>(p, stream);
+        return bias ? launch_variant<64, C, kBiasGeneral, NORM, true, true, GLIST>(p, stream)
+                    : launch_variant<64, C, kBiasNone, NORM, true, true, GLIST>(p, stream);
     });
 }
 

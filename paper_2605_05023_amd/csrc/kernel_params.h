@@ -7,6 +7,9 @@
 #include "fastdiv.h"
 #include "plan.h"
 
+// Largest listed global set of the global sliding window (staged in LDS).
+constexpr int kMaxGlobalList = 2048;
+
 struct AttnParams {
     const void* q;
     const void* k;
@@ -48,7 +51,9 @@ struct AttnParams {
     KeyBand band;            // closed-form masks as a key band
     // Masks whose visible keys come from per-row data (general path).
     int32_t mask_kind;       // attn_mask_kind_t
-    int32_t num_global;      // global sliding window: positions 0..num_global-1
+    int32_t num_global;      // global sliding window: size of G
+    const int32_t* gtok;     // G as a sorted list of positions (device), or null for
+                             // positions 0..num_global-1
     const int32_t* seg;      // segment start positions (device), or null
     int32_t num_seg;
     int32_t query_start;     // causal blockwise: first test-query position

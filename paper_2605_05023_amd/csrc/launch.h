@@ -17,6 +17,10 @@ hipError_t launch_bf16_closed_form_d64(const AttnParams& p, hipStream_t stream);
 hipError_t launch_bf16_general_softmax(const AttnParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_bf16_general_relu(const AttnParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_bf16_general_sigmoid(const AttnParams& p, int head_dim, hipStream_t stream);
+// general path with a listed global set (global sliding window), per normalisation
+hipError_t launch_bf16_glist_softmax(const AttnParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_bf16_glist_relu(const AttnParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_bf16_glist_sigmoid(const AttnParams& p, int head_dim, hipStream_t stream);
 
 // fp32 inputs and arithmetic; head_dim 64 or 128.
 hipError_t launch_f32(const AttnParams& p, int head_dim, hipStream_t stream);

@@ -96,3 +96,23 @@ ATTN_HD RowVis row_visibility(int32_t kind, KeyBand band, int32_t num_global, co
 
 // Is key j visible under `r`?
 ATTN_HD bool row_sees(RowVis r, int32_t j) { return j < r.pfx || (j >= r.jlo && j <= r.jhi); }
+
+// Global sliding window with G given as a sorted list g of ng positions: a row
+// whose key-axis position is in G sees every key; any other row sees its
+// window band here, and the keys of G outside that band are taken separately
+// (they are not a prefix, so they do not fit the prefix + band form).
+ATTN_HD RowVis row_vis_listed(KeyBand band, const int32_t* g, int32_t ng, int32_t i, int32_t lq,
+                              int32_t lk)
+{
+    RowVis r = {0, 1, 0};
+    if (lk <= 0) return r;
+    const int32_t ip = i + (lk - lq);
+    const int32_t k = ip >= 0 ? segment_of(g, ng, ip) : -1;
+    if (k >= 0 && g[k] == ip) {
+        r.jlo = 0;
+        r.jhi = lk - 1;
+    } else {
+        band_row(band, i, lq, lk, &r.jlo, &r.jhi);
+    }
+    return r;
+}

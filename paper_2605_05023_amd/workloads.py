@@ -65,6 +65,7 @@ class Workload:
     len_hi: int = 0
     prefix_len: int = 0        # PrefixLM L_p; share question: prompt length
     num_global: int = 0        # global sliding window: positions 0..num_global-1
+    global_list: tuple = ()    # global sliding window: G as listed positions (overrides num_global)
     num_segments: int = 0      # share question responses / blockwise documents
     query_start: int = 0       # causal blockwise L_q
     relpos: bool = False       # relative position term (i - j)
@@ -108,6 +109,12 @@ NEXT_WORKLOADS = {
                            softcap=50.0, norm="sigmoid"),
     "global_window_bf16": _llama7b("global_window_bf16", 10, mask=MASK_GLOBAL_WINDOW,
                                    window_left=512, window_right=512, num_global=16),
+    # the same window with a scattered global set: a leading token, a few in
+    # the middle, the last one
+    "global_window_listed_bf16": _llama7b("global_window_listed_bf16", 13,
+                                          mask=MASK_GLOBAL_WINDOW, window_left=512,
+                                          window_right=512,
+                                          global_list=(0, 5, 300, 2049, 4096, 6000, 8191)),
     "share_question_bf16": _llama7b("share_question_bf16", 11, mask=MASK_SHARE_QUESTION,
                                     prefix_len=2048, num_segments=4),
     "causal_blockwise_bf16": _llama7b("causal_blockwise_bf16", 12, mask=MASK_CAUSAL_BLOCKWISE,
@@ -160,6 +167,10 @@ class Inputs:
         if self.segment_starts is not None:
             seg = self.segment_starts
             kw["segment_starts"] = seg.to(device) if device is not None else seg
+        if wl.global_list:
+            g = torch.tensor(wl.global_list, dtype=torch.int32)
+            kw["global_tokens"] = g.to(device) if device is not None else g
+            kw["num_global"] = 0
         if self.cu_seqlens is not None:
             cu = self.cu_seqlens.to(device) if device is not None else self.cu_seqlens
             kw.update(cu_seqlens_q=cu, cu_seqlens_k=cu, max_seqlen_q=self.max_seqlen,
@@ -174,7 +185,8 @@ class Inputs:
         kw = dict(prefix_len=wl.prefix_len, relpos=wl.relpos, norm=NORM_CODES[wl.norm],
                   query_start=wl.query_start)
         if wl.mask == MASK_GLOBAL_WINDOW:
-            kw["global_tokens"] = list(range(wl.num_global))
+            kw["global_tokens"] = list(wl.global_list) if wl.global_list else \
+                list(range(wl.num_global))
         if self.segment_starts is not None:
             S = self.max_seqlen
             ids = [-1] * S

@@ -249,3 +249,16 @@ def test_broadcast_inputs_accepted(lib):
     d.stride_k_h = 0
     d.stride_v_h = 0
     assert call(lib, d, q=None) == err("ATTN_ERR_NULL_PTR")
+
+
+def test_row_range_rejects_listed_global_set(lib):
+    d = base_desc()
+    d.mask_kind = _abi.ATTN_MASK_GLOBAL_SLIDING_WINDOW
+    d.window_left = d.window_right = 4
+    d.num_global = 3
+    d.global_tokens = P  # never dereferenced
+    out = (ctypes.c_int32 * 3)()
+    assert lib.attn_row_range(ctypes.byref(d), None, 0, 10, 10, out) == err("ATTN_ERR_UNSUPPORTED")
+    d.global_tokens = None  # leading run: prefix plus band
+    assert lib.attn_row_range(ctypes.byref(d), None, 5, 10, 10, out) == 0
+    assert tuple(out) == (0, 0, 9)  # prefix {0,1,2} touches the band [1, 9]: merged

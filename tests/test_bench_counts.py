@@ -16,7 +16,8 @@ import bench  # noqa: E402
 from paper_2605_05023_amd.workloads import WORKLOADS, make_inputs  # noqa: E402
 
 NAMES = ["causal_bf16", "gqa_swa_bf16", "alibi_softcap_bf16", "prefixlm_bf16",
-         "global_window_bf16", "share_question_bf16", "causal_blockwise_bf16", "relu_bf16"]
+         "global_window_bf16", "global_window_listed_bf16", "share_question_bf16",
+         "causal_blockwise_bf16", "relu_bf16"]
 
 
 @pytest.mark.parametrize("name", NAMES)

@@ -66,6 +66,30 @@ SMALL = [
       window_right=30, num_global=0),
     W("global_d128_wide_g", "bf16", 1, 2, 2, 333, 128, MASK_GLOBAL_WINDOW, window_left=8,
       window_right=64, num_global=140),
+    # global sliding window with a listed global set (gathered tiles): scattered
+    # positions, positions inside and outside the band, a tile-sized run, the
+    # last key, positions past the end, a single entry
+    W("glist_d128", "bf16", 2, 2, 2, 300, 128, MASK_GLOBAL_WINDOW, window_left=20,
+      window_right=20, global_list=(0, 5, 150, 299)),
+    W("glist_d64_gqa_one_sided", "bf16", 2, 8, 2, 333, 64, MASK_GLOBAL_WINDOW, window_left=40,
+      window_right=0, global_list=(3, 64, 65, 200, 330, 500)),
+    W("glist_d128_run_of_70", "bf16", 1, 4, 4, 400, 128, MASK_GLOBAL_WINDOW, window_left=8,
+      window_right=8, global_list=tuple(range(100, 170)) + (399,)),
+    W("glist_d128_single_w0", "bf16", 1, 2, 2, 200, 128, MASK_GLOBAL_WINDOW, window_left=0,
+      window_right=0, global_list=(77,)),
+    W("glist_d64_alibi_relpos_softcap", "bf16", 1, 4, 4, 260, 64, MASK_GLOBAL_WINDOW,
+      window_left=16, window_right=16, global_list=(1, 128, 250), alibi=True, relpos=True,
+      softcap=30.0, sigma=1.5),
+    W("glist_d128_relpos", "bf16", 1, 2, 2, 300, 128, MASK_GLOBAL_WINDOW, window_left=10,
+      window_right=5, global_list=(2, 100, 290), relpos=True),
+    W("glist_d128_sigmoid", "bf16", 1, 2, 2, 300, 128, MASK_GLOBAL_WINDOW, window_left=30,
+      window_right=30, global_list=(0, 64, 200), norm="sigmoid"),
+    W("glist_d64_relu_softcap", "bf16", 1, 3, 3, 220, 64, MASK_GLOBAL_WINDOW, window_left=12,
+      window_right=12, global_list=(10, 11, 190), norm="relu", softcap=20.0),
+    W("fp32_glist", "fp32", 1, 2, 2, 150, 64, MASK_GLOBAL_WINDOW, window_left=10,
+      window_right=10, global_list=(4, 70, 149)),
+    W("fp32_glist_d128_relpos", "fp32", 1, 2, 2, 130, 128, MASK_GLOBAL_WINDOW, window_left=5,
+      window_right=5, global_list=(0, 40, 41, 100), relpos=True),
     # share question (general path)
     W("share_d128", "bf16", 2, 2, 2, 300, 128, MASK_SHARE_QUESTION, prefix_len=64,
       num_segments=3),
@@ -110,6 +134,11 @@ def test_small_next(wl):
 
 VARLEN = [
     W("varlen_prefix", "bf16", 4, 4, 2, 0, 128, MASK_PREFIX_LM, prefix_len=50),
+    # listed global positions are per sequence; those past a sequence's end are ignored
+    W("varlen_glist", "bf16", 4, 4, 2, 0, 128, MASK_GLOBAL_WINDOW, window_left=16,
+      window_right=16, global_list=(0, 6, 129, 250)),
+    W("varlen_glist_fp32", "fp32", 4, 2, 2, 0, 64, MASK_GLOBAL_WINDOW, window_left=8,
+      window_right=8, global_list=(3, 100, 200)),
     W("varlen_share", "bf16", 3, 2, 2, 0, 128, MASK_SHARE_QUESTION, prefix_len=40,
       num_segments=3),
     W("varlen_relu_relpos", "bf16", 3, 4, 4, 0, 64, MASK_CAUSAL, norm="relu", relpos=True),

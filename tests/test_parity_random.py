@@ -60,10 +60,19 @@ def _draw_cases(n=48, seed=2605):
         name = (f"s{seed}_r{i:02d}_{dtype}_d{D}_g{group}x{hkv}_b{B}_{'varlen' if varlen else f's{S}'}"
                 f"_{MASK_NAMES[mask]}{'_alibi' if alibi else ''}{'_relpos' if relpos else ''}"
                 f"{f'_cap{softcap:g}' if softcap else ''}{'' if norm == 'softmax' else '_' + norm}")
+        wseed = int(rng.integers(0, 1 << 30))
+        if mask == MASK_GLOBAL_WINDOW:
+            # half of them list G instead (sorted positions, some past the end),
+            # drawn from the case's own generator so the other cases stay put
+            g = np.random.default_rng(wseed + 1)
+            if g.random() < 0.5:
+                n = int(g.integers(1, 12))
+                kw["global_list"] = tuple(sorted(g.choice(S + 20, size=min(n, S + 20),
+                                                          replace=False).tolist()))
+                name += "_listed"
         wl = Workload(name, dtype, B, hq, hkv, 0 if varlen else S, D, mask=mask, alibi=alibi,
                       relpos=relpos, softcap=softcap, norm=norm, sigma=sigma,
-                      seed=int(rng.integers(0, 1 << 30)), varlen=varlen, len_lo=0,
-                      len_hi=S, **kw)
+                      seed=wseed, varlen=varlen, len_lo=0, len_hi=S, **kw)
         cases.append(wl)
     return cases
 

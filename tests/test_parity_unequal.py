@@ -63,6 +63,10 @@ def _draw(n=40, seed=4411):
                             int(rng.choice([-1, 0, int(rng.integers(0, 40))])))
             if mask == MASK_GLOBAL_WINDOW:
                 kw["num_global"] = int(rng.integers(0, 12))
+                g = np.random.default_rng(kw["num_global"] * 7919 + i)
+                if g.random() < 0.5:  # G listed: sorted positions, some past the end
+                    kw["global_list"] = sorted(g.choice(maxk + 20, size=min(6, maxk + 20),
+                                                        replace=False).tolist())
         if mask == MASK_PREFIX_LM:
             kw["prefix_len"] = int(rng.integers(0, maxk + 1))
         if mask in (MASK_SHARE_QUESTION, MASK_CAUSAL_BLOCKWISE):
@@ -133,7 +137,10 @@ def test_unequal_lengths_random(c):
     if "segments" in c:
         gkw["segment_starts"] = torch.tensor(c["segments"], dtype=torch.int32, device=dev)
         okw["token_ids"] = _token_ids(c["segments"], max(maxk, 1))
-    if c["mask"] == MASK_GLOBAL_WINDOW:
+    if c["mask"] == MASK_GLOBAL_WINDOW and "global_list" in c:
+        gkw["global_tokens"] = torch.tensor(c["global_list"], dtype=torch.int32, device=dev)
+        okw["global_tokens"] = list(c["global_list"])
+    elif c["mask"] == MASK_GLOBAL_WINDOW:
         gkw["num_global"] = c["num_global"]
         okw["global_tokens"] = list(range(c["num_global"]))
     o, lse = None, None
