@@ -102,9 +102,18 @@ struct Traits {
     static constexpr bool SOFTCAP = CAP_ != kCapOff, MODS = SOFTCAP || BIAS_ != kBiasNone;
     static constexpr int BIAS = BIAS_, NORM = NORM_;
     static constexpr bool SOFTMAX = NORM_ == kNormSoftmax, GEN = GEN_, LEFT = LEFT_ || GEN_;
-    // softmax without score mods whose rows all see the first visited tile
-    // (no left bound): running max checked through the row sums
-    static constexpr bool MAXFREE = SOFTMAX && !MODS && !LEFT;
+    // softmax without a left bound on the visible keys: P of a tile is made
+    // with the running max as it stands and checked through the row sums
+    // (check_tile); the first visited tile's max starts the running max
+    static constexpr bool MAXFREE = SOFTMAX && !LEFT;
+    // MAXFREE with score mods: the running max is folded into every score's
+    // additive constant, so the exponential takes the score as it stands
+    static constexpr bool FOLD = MAXFREE && MODS;
+    // ALiBi without a left bound: key tiles are visited from the workgroup's
+    // diagonal (where the row maxima lie) down to the first tile, then up to
+    // the last, and check-free tiles on one side of every row take |i' - j|
+    // as a per-tile constant plus the key's offset
+    static constexpr bool DIAG = MAXFREE && BIAS_ == kBiasAlibi;
     // softmax with soft-cap or ALiBi, or on the general (index-mask) path: O
     // is normalised by the sum of P as rounded to bf16 (ALiBi makes rows
     // local, index masks leave some rows few keys; there the rounding of a
@@ -378,6 +387,53 @@ __device__ __forceinline__ float final_score(float x, const AttnParams& p, const
                                               pb.lin - (float)c);
 }
 
+// Side of a key tile relative to every row of the workgroup (DIAG): all its
+// keys at or before every row's key-axis position, all at or after, or
+// neither (or not known).
+enum : int { kSideBoth = 0, kSideLeft = 1, kSideRight = 2 };
+
+// FOLD: this lane's additive constant of a tile's scores: the short soft-cap
+// form's C' (it ends in C' - 2C'/(1 + e)), minus the running max m_base, plus
+// the per-tile part of the position terms (ALiBi on one-sided tiles, the
+// relative position term always).
+template <class T, int SIDE>
+__device__ __forceinline__ float fold_const(const WaveState<T>& ws, const AttnParams& p,
+                                            const PosBase& pb, float m_base)
+{
+    float a = (T::CAP == kCapShort ? p.softcap_post_u : 0.0f) - m_base;
+    if constexpr (T::BIAS == kBiasAlibi && SIDE == kSideLeft) a = __builtin_fmaf(ws.bias_abs, pb.abs, a);
+    if constexpr (T::BIAS == kBiasAlibi && SIDE == kSideRight) a = __builtin_fmaf(-ws.bias_abs, pb.abs, a);
+    if constexpr (T::BIAS == kBiasRelPos) a = __builtin_fmaf(ws.bias_lin, pb.lin, a);
+    return a;
+}
+
+// FOLD: the final score of element offset c minus the running max, from the
+// raw dot product and the tile constant a of fold_const.
+template <class T, int SIDE>
+__device__ __forceinline__ float fold_score(float dot, float a, const AttnParams& p,
+                                            const WaveState<T>& ws, const PosBase& pb, int c)
+{
+    float u;
+    if constexpr (T::CAP == kCapShort) {
+        const float e = __builtin_amdgcn_exp2f(dot * p.softcap_pre2);
+        u = __builtin_fmaf(-2.0f * p.softcap_post_u, __builtin_amdgcn_rcpf(1.0f + e), a);
+    } else if constexpr (T::CAP == kCapExact) {
+        u = softcap_u(dot, p.softcap_pre, p.softcap_post_u) + a;
+    } else {
+        u = __builtin_fmaf(dot, p.scale_u, a);
+    }
+    if constexpr (T::BIAS == kBiasAlibi) {
+        if constexpr (SIDE == kSideLeft)  // |i' - j| = base - c
+            u = __builtin_fmaf((float)c, -ws.bias_abs, u);
+        else if constexpr (SIDE == kSideRight)  // |i' - j| = c - base
+            u = __builtin_fmaf((float)c, ws.bias_abs, u);
+        else
+            u = __builtin_fmaf(ws.bias_abs, __builtin_fabsf(pb.abs - (float)c), u);
+    }
+    if constexpr (T::BIAS == kBiasRelPos) u = __builtin_fmaf((float)c, -ws.bias_lin, u);
+    return u;
+}
+
 // S^T = K Q^T for the K tile in LDS at `kt`.
 template <class T>
 __device__ __forceinline__ void qk_tile(const char* kt, const WaveState<T>& ws, f32x16 (&s)[T::NB])
@@ -434,10 +490,12 @@ __device__ __forceinline__ float mods_and_max(f32x16 (&s)[T::NB], const AttnPara
 
 // Norm of one score (in units; raw dot product when there are no mods):
 // softmax exp2(S - m), or the ReLU / Sigmoid activation of the natural score.
-template <class T>
+// SHIFT = false (FOLD): the score already has the running max taken off.
+template <class T, bool SHIFT = true>
 __device__ __forceinline__ float norm_value(float x, float m_use, float scale_u)
 {
     if constexpr (T::SOFTMAX) {
+        if constexpr (T::FOLD && !SHIFT) return __builtin_amdgcn_exp2f(x);
         return __builtin_amdgcn_exp2f(T::MODS ? x - m_use : __builtin_fmaf(x, scale_u, -m_use));
     } else {
         return activation<T::NORM>(T::MODS ? x : x * scale_u);
@@ -492,7 +550,7 @@ struct RowSums {
 
 // P = Norm(S) as bf16 B operands of the P V product; returns (softmax) this
 // lane's partial row sums.
-template <class T>
+template <class T, bool SHIFT = true>
 __device__ __forceinline__ RowSums exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2],
                                             float m_use, float scale_u)
 {
@@ -503,8 +561,8 @@ __device__ __forceinline__ RowSums exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw
         for (int u = 0; u < 2; ++u) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                float p0 = norm_value<T>(s[b][8 * u + 2 * q], m_use, scale_u);
-                float p1 = norm_value<T>(s[b][8 * u + 2 * q + 1], m_use, scale_u);
+                float p0 = norm_value<T, SHIFT>(s[b][8 * u + 2 * q], m_use, scale_u);
+                float p1 = norm_value<T, SHIFT>(s[b][8 * u + 2 * q + 1], m_use, scale_u);
                 pw[b][u][q] = pack_bf16(p0, p1);
                 if constexpr (T::SOFTMAX) {
                     rs.f += p0;
@@ -550,6 +608,9 @@ __device__ __forceinline__ void check_tile(WaveState<T>& ws, const f32x16 (&s)[T
         tm = pair_max(tm);
         if constexpr (!T::MODS) tm *= p.scale_u;  // raw max -> units (scale > 0)
         const float m_old = ws.m_run;
+        // FOLD: the scores carry -m_old (-0 while the row has seen no key)
+        const float m_base = T::FOLD && m_old != -__builtin_inff() ? m_old : 0.0f;
+        if constexpr (T::FOLD) tm += m_base;
         const float m_new = need_row ? __builtin_fmaxf(m_old, tm) : m_old;
         const float alpha =
             need_row && m_old != -__builtin_inff() ? __builtin_amdgcn_exp2f(m_old - m_new) : 1.0f;
@@ -560,7 +621,8 @@ __device__ __forceinline__ void check_tile(WaveState<T>& ws, const f32x16 (&s)[T
         for (int d = 0; d < T::DBLK; ++d)
 #pragma unroll
             for (int e = 0; e < 16; ++e) ws.oacc[d][e] *= alpha;
-        rs = exp_tile<T>(s, pw, m_new == -__builtin_inff() ? 0.0f : m_new, p.scale_u);
+        rs = exp_tile<T, true>(s, pw, (m_new == -__builtin_inff() ? 0.0f : m_new) - m_base,
+                               p.scale_u);
     }
     ws.l_run += rs.f;
     ws.l_o += rs.b;
@@ -601,7 +663,7 @@ __device__ __forceinline__ void pv_tile(const char* vt, const u32x4 (&pw)[T::NB]
 // vector work runs while the matrix cores are busy and LDS latency stays
 // hidden. The QK^T products run block by block, each accumulation chain
 // issued back to back, the order that measured fastest.
-template <class T, bool MASKED, class LOADER>
+template <class T, bool MASKED, int SIDE, class LOADER>
 __device__ __forceinline__ void pipelined_step(const char* kread, const char* vread,
                                                WaveState<T>& ws, const f32x16 (&sc)[T::NB],
                                                f32x16 (&sn)[T::NB], const AttnParams& p,
@@ -650,8 +712,8 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
         if constexpr (i % LSTEP == 0) load(i / LSTEP);
         static_for<EQ / 2>([&](auto kc) __attribute__((always_inline)) {
             constexpr int el = i * EQ + 2 * kc.value, bb = el / 16, e = el % 16;
-            const float p0 = norm_value<T>(sc[bb][e], m_use, p.scale_u);
-            const float p1 = norm_value<T>(sc[bb][e + 1], m_use, p.scale_u);
+            const float p0 = norm_value<T, !T::FOLD>(sc[bb][e], m_use, p.scale_u);
+            const float p1 = norm_value<T, !T::FOLD>(sc[bb][e + 1], m_use, p.scale_u);
             pw[bb][e / 8][(e % 8) / 2] = pack_bf16(p0, p1);
             if constexpr (T::SOFTMAX) {
                 rs.f += p0;
@@ -664,6 +726,10 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     check_tile<T>(ws, sc, pw, rs, p, jc);
     const MaskThr mt = mask_thresholds(ws, jn);
     const PosBase pb = pos_base(ws, jn);
+    // FOLD: the next tile's scores take off the running max as it now stands
+    float fa = 0.0f;
+    if constexpr (T::FOLD)
+        fa = fold_const<T, SIDE>(ws, p, pb, ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run);
     static_for<PV>([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = ic.value;
         constexpr int b = i / (2 * DBLK), u = (i / DBLK) % 2, d = i % DBLK;
@@ -678,7 +744,10 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             // element (bb, e) is key jn + 8lh + c, c = 32bb + e + (e >= 8 ? 8 : 0)
             constexpr int c = 32 * bb + e + (e >= 8 ? 8 : 0);
             float x = sn[bb][e];
-            if constexpr (T::MODS) x = final_score<T>(x, p, ws, pb, c);
+            if constexpr (T::FOLD)
+                x = fold_score<T, SIDE>(x, fa, p, ws, pb, c);
+            else if constexpr (T::MODS)
+                x = final_score<T>(x, p, ws, pb, c);
             if constexpr (MASKED)
                 if (!visible<T>(mt, c)) x = -__builtin_inff();
             sn[bb][e] = x;
@@ -702,7 +771,7 @@ __device__ __forceinline__ void last_step(const char* vread, WaveState<T>& ws, f
     // under causal-like masks): P is zero, nothing to add.
     if (!__builtin_amdgcn_ballot_w64(row_sees_tile(ws, jc))) return;
     u32x4 pw[T::NB][2];
-    const RowSums rs = exp_tile<T>(sc, pw, m_use, p.scale_u);
+    const RowSums rs = exp_tile<T, !T::FOLD>(sc, pw, m_use, p.scale_u);
     check_tile<T>(ws, sc, pw, rs, p, jc);
     pv_tile<T>(vread, pw, ws);
 }
@@ -1005,6 +1074,21 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         jbeg = gp.lo;
         jend = gp.hi;
     }
+    // DIAG: visited tiles, as virtual indices n = 0 .. hi - lo - 1, run from
+    // the tile of the workgroup's last row down to lo, then from there up
+    // (tile_of below); a tile is left of every row when its last key is at or
+    // before the first row's key-axis position, right when its first key is
+    // at or after the last row's.
+    int t_diag = 0, n_desc = 0, ip_first = 0, ip_last = 0;
+    if constexpr (T::DIAG) {
+        ip_first = q0 + (lk - lq);
+        ip_last = min(q0 + p.wg_rows, lq) - 1 + (lk - lq);
+        t_diag = min(max(ip_last, 0) / BN, gp.hi - 1);
+        if (t_diag < gp.lo) t_diag = gp.lo;
+        n_desc = t_diag - gp.lo + 1;
+        jbeg = 0;
+        jend = gp.hi - gp.lo;
+    }
     // Relative-position reference: the row's first visible key for softmax
     // (largest bias; the shift is added back to the LSE), i' otherwise.
     ws.jref = T::SOFTMAX ? (ws.pfx > 0 ? 0 : ws.jlo) : ws.ip;
@@ -1034,8 +1118,17 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     auto tile_of = [&](int n) __attribute__((always_inline)) -> int {
         if constexpr (T::GEN)
             return n < tr.len1 ? tr.r1_lo + n : tr.r2_lo + (n - tr.len1);
+        else if constexpr (T::DIAG)
+            return n < n_desc ? t_diag - n : gp.lo + n;
         else
             return n;
+    };
+    // DIAG: class of a tile: masked (any side), or check-free on the given side
+    auto diag_class = [&](int t) __attribute__((always_inline)) -> int {
+        if (!(t >= gp.full_lo && t < gp.full_hi)) return 0;
+        if ((t + 1) * BN - 1 <= ip_first) return 1 + kSideLeft;
+        if (t * BN >= ip_last) return 1 + kSideRight;
+        return 1 + kSideBoth;
     };
     auto gen_full = [&](int t) __attribute__((always_inline)) -> bool {
         return (t + 1) * BN <= tr.pmin || (tr.lomax <= t * BN && t * BN + BN - 1 <= tr.himin);
@@ -1067,15 +1160,24 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             ws.m_run = mx;
         else
             update_max(ws, mx);
+        if constexpr (T::FOLD) {  // take the running max off the first tile's scores
+            const float mb = mx == -__builtin_inff() ? 0.0f : mx;
+#pragma unroll
+            for (int b = 0; b < T::NB; ++b)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) ws.sa[b][e] -= mb;
+        }
         __syncthreads();  // K buffer 0 is reloaded in the first iteration
 
         // Iteration j with parity PAR = (j - jbeg) & 1 reads K_{j+1} from K
         // buffer PAR^1 and V_j from V buffer PAR, and loads K_{j+2} into K
         // buffer PAR and V_{j+1} into V buffer PAR^1 (j counts visited
         // tiles). MASKED is the class of tile j+1.
-        auto iteration = [&](auto par_c, auto masked_c, int j) __attribute__((always_inline)) {
+        auto iteration = [&](auto par_c, auto masked_c, auto side_c, int j)
+                             __attribute__((always_inline)) {
             constexpr int PAR = decltype(par_c)::value;
             constexpr bool MASKED = decltype(masked_c)::value;
+            constexpr int SIDE = decltype(side_c)::value;
             char* kread = PAR ? lds_k0 : lds_k1;
             char* kwrite = PAR ? lds_k1 : lds_k0;
             char* vread = PAR ? lds_v1 : lds_v0;
@@ -1092,34 +1194,36 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             };
             const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
             if constexpr (PAR == 0)
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sa, ws.sb, p, m_use, tile_of(j) * BN,
-                                          t1 * BN, load);
+                pipelined_step<T, MASKED, SIDE>(kread, vread, ws, ws.sa, ws.sb, p, m_use,
+                                                tile_of(j) * BN, t1 * BN, load);
             else
-                pipelined_step<T, MASKED>(kread, vread, ws, ws.sb, ws.sa, p, m_use, tile_of(j) * BN,
-                                          t1 * BN, load);
+                pipelined_step<T, MASKED, SIDE>(kread, vread, ws, ws.sb, ws.sa, p, m_use,
+                                                tile_of(j) * BN, t1 * BN, load);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
         };
         // Loop splitting (Section 3.4): runs of partial and check-free tiles,
         // each phase with a branch-free body.
         int j = jbeg, par = 0;
-        auto phase = [&](auto masked_c, int end) __attribute__((always_inline)) {  // iterations while tile j+1 < end
+        // iterations while tile j+1 < end, with the side of those tiles
+        auto phase = [&](auto masked_c, int end, auto side_c) __attribute__((always_inline)) {
             if (par && j + 1 < end) {
-                iteration(Parity<1>{}, masked_c, j);
+                iteration(Parity<1>{}, masked_c, side_c, j);
                 ++j;
                 par = 0;
             }
             while (j + 2 < end) {
-                iteration(Parity<0>{}, masked_c, j);
-                iteration(Parity<1>{}, masked_c, j + 1);
+                iteration(Parity<0>{}, masked_c, side_c, j);
+                iteration(Parity<1>{}, masked_c, side_c, j + 1);
                 j += 2;
             }
             if (j + 1 < end) {
-                iteration(Parity<0>{}, masked_c, j);
+                iteration(Parity<0>{}, masked_c, side_c, j);
                 ++j;
                 par = 1;
             }
         };
+        using Both = std::integral_constant<int, kSideBoth>;
         if constexpr (T::GEN) {
             // Visited tiles fall into at most four runs: check-free prefix
             // tiles, partial tiles, check-free band tiles, partial tiles. Any
@@ -1133,14 +1237,35 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             const int e1 = run_end(jbeg + 1, true);
             const int e2 = run_end(e1, false);
             const int e3 = run_end(e2, true);
-            phase(Bool<false>{}, e1);
-            phase(Bool<true>{}, e2);
-            phase(Bool<false>{}, e3);
-            phase(Bool<true>{}, jend);
+            phase(Bool<false>{}, e1, Both{});
+            phase(Bool<true>{}, e2, Both{});
+            phase(Bool<false>{}, e3, Both{});
+            phase(Bool<true>{}, jend, Both{});
+        } else if constexpr (T::DIAG) {
+            // In visiting order: tiles around the diagonal (partial or
+            // check-free on neither side), check-free tiles left of every row,
+            // partial ones at the low end, check-free tiles right of every
+            // row, partial ones at the high end. Each phase takes the run of
+            // its class that starts at the next tile; the masked body, which
+            // is correct for every tile, finishes whatever remains.
+            auto run_end = [&](int from, int cls) __attribute__((always_inline)) {
+                int e = from;
+                while (e < jend && diag_class(tile_of(e)) == cls) ++e;
+                return e;
+            };
+            using Left = std::integral_constant<int, kSideLeft>;
+            using Right = std::integral_constant<int, kSideRight>;
+            phase(Bool<true>{}, run_end(j + 1, 0), Both{});
+            phase(Bool<false>{}, run_end(j + 1, 1 + kSideBoth), Both{});
+            phase(Bool<true>{}, run_end(j + 1, 0), Both{});
+            phase(Bool<false>{}, run_end(j + 1, 1 + kSideLeft), Left{});
+            phase(Bool<true>{}, run_end(j + 1, 0), Both{});
+            phase(Bool<false>{}, run_end(j + 1, 1 + kSideRight), Right{});
+            phase(Bool<true>{}, jend, Both{});
         } else {
-            phase(Bool<true>{}, gp.full_lo);
-            phase(Bool<false>{}, gp.full_hi);
-            phase(Bool<true>{}, jend);
+            phase(Bool<true>{}, gp.full_lo, Both{});
+            phase(Bool<false>{}, gp.full_hi, Both{});
+            phase(Bool<true>{}, jend, Both{});
         }
         rescale_if_needed(ws);
         const float m_use = ws.m_run == -__builtin_inff() ? 0.0f : ws.m_run;
