@@ -372,6 +372,26 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.softcap_pre = d.softcap > 0.0f ? d.scale / d.softcap : 0.0f;
     p.softcap_pre2 = p.softcap_pre * (float)(2.0 * 1.4426950408889634);
     p.softcap_post_u = d.softcap * p.unit;
+    {
+        // tanh(y) / y ~= a0 + a1 y^2 + a2 y^4 + a3 y^6 on |y| <= 1/2: Remez
+        // fit of the relative error (max 5.5e-7) in y^2 over [0, 1/4]. With
+        // s = scale / C the soft-cap is C' tanh(s dot) = dot sum_k b_k dot^(2k),
+        // b_k = C' s^(2k+1) a_k, valid while dot^2 <= (1 / (2 s))^2.
+        static const double a[4] = {0.99999946, -0.33326318, 0.13190297, -0.04440223};
+        p.cap_zmax = -1.0f;  // no polynomial (kernels take the exact form)
+        if (d.softcap > 0.0f) {
+            const double sc = (double)d.scale / d.softcap, cu = (double)p.softcap_post_u;
+            bool normal = true;
+            double sk = sc;
+            for (int k = 0; k < 4; ++k) {
+                p.cap_poly[k] = (float)(cu * sk * a[k]);
+                normal = normal && std::fabs(p.cap_poly[k]) >= 1.1754943508222875e-38;
+                sk *= sc * sc;
+            }
+            const double zmax = 0.25 / (sc * sc);
+            if (normal) p.cap_zmax = zmax < 3.0e38 ? (float)zmax : 3.0e38f;
+        }
+    }
     // Longest tiles first: the last query tiles under causal-like masks, the
     // first ones when global rows (which see every key) sit at the start.
     p.q_order = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.num_global > 0 ? 1 : 0;
@@ -432,6 +452,25 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         p.div_chunk_full = make_fastdiv((uint32_t)(p.chunk * gsets));
         p.div_chunk_last = make_fastdiv((uint32_t)(last_groups * gsets));
         p.last_chunk = (int32_t)last;
+    }
+    // bf16 variable-length batch walked one kv group at a time per XCD: a
+    // packed grid of only the query spans each sequence has. An XCD's groups
+    // hold at most ceil(hkv / 8) kv heads of any one sequence, so their spans
+    // number at most ceil(hkv / 8) * total_q / 128 + (groups per XCD).
+    p.grid = (int32_t)blocks;
+    p.compact = 0;
+    p.groups_per_xcd = 0;
+    p.items_per_span = gsets * hp;
+    if (d.dtype == ATTN_BF16 && varlen && p.map_mode == 1 && p.chunk == 1) {
+        const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
+        const int64_t per_seq = (d.num_kv_heads + 7) / 8;
+        const int64_t spans = per_seq * d.total_q / 128 + groups_per_xcd;
+        const int64_t packed = 8 * spans * gsets * hp;
+        if (packed < blocks) {
+            p.compact = 1;
+            p.groups_per_xcd = (int32_t)groups_per_xcd;
+            p.grid = (int32_t)packed;
+        }
     }
     const bool glist = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.global_tokens &&
                        d.num_global > 0;

@@ -114,6 +114,11 @@ struct Traits {
     // the last, and check-free tiles on one side of every row take |i' - j|
     // as a per-tile constant plus the key's offset
     static constexpr bool DIAG = MAXFREE && BIAS_ == kBiasAlibi;
+    // FOLD with the short soft-cap form: the pipelined steps take the soft-cap
+    // of a tile from an odd polynomial in the dot product while every |y| of
+    // the tile (y = scale * dot / C) stays within its range, and recompute the
+    // tile with the short form otherwise (fold_score)
+    static constexpr bool POLY = FOLD && CAP_ == kCapShort;
     // softmax with soft-cap or ALiBi, or on the general (index-mask) path: O
     // is normalised by the sum of P as rounded to bf16 (ALiBi makes rows
     // local, index masks leave some rows few keys; there the rounding of a
@@ -183,7 +188,10 @@ __device__ __forceinline__ uint32_t load_lane_offset(int wave, int lane, int64_t
 // Issue the direct global->LDS loads of one tile: rows j0..j0+BN-1 of the
 // slice described by `rs` (whose range ends at the sequence end, so rows past
 // it read as zero). The row offset is wave-uniform and added to the lane's
-// constant byte offset.
+// constant byte offset. (Advancing the descriptor's base by the row offset
+// instead, as scalar work, measured 1-2.5 % slower: seven scalar
+// instructions per load in the wave's in-order stream against one vector
+// add.)
 template <class T>
 __device__ __forceinline__ void issue_load(char* lds_tile, __amdgpu_buffer_rsrc_t rs, int j0,
                                            uint32_t row_bytes, uint32_t lane_off, int wave, int p)
@@ -236,7 +244,8 @@ __device__ __forceinline__ float pair_sum(float x)
     return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
 }
 
-// Sequence, first query head of the workgroup's head set, kv head, query tile.
+// Sequence, first query head of the workgroup's head set, kv head, query
+// tile; qt < 0: no work item (past the end of a packed grid).
 struct WorkItem {
     int b, hq, hkv, qt;
 };
@@ -279,12 +288,66 @@ struct Bool {
 // inside it), so the K/V tiles in use at any moment belong to a few groups
 // and stay in the L2 instead of cycling every group's K/V through the
 // caches once per tile.
+// Packed variable-length grid (compact, with mode 1 and one kv group per
+// chunk): an XCD's work items are those of its groups g = x + 8 i in order i,
+// each group contributing only the query spans of its own sequence
+// (ceil(length / 128) spans of hp tiles, times its head sets), in the same
+// order inside the group as the padded grid, so no workgroup is spent on
+// tiles past a sequence's end. Every wave finds its group from the prefix
+// sums of the item counts over the XCD's groups, 64 groups at a time.
+__device__ __forceinline__ WorkItem decode_packed(const AttnParams& p, uint32_t uw)
+{
+    WorkItem it = {0, 0, 0, -1};
+    const uint32_t x = uw & 7, k = uw >> 3;
+    const int lane = __lane_id();
+    uint32_t base = 0;  // items of the groups before this block of 64
+    for (int i0 = 0; i0 < p.groups_per_xcd; i0 += 64) {
+        const int i = i0 + lane;
+        uint32_t n = 0, b = 0, spans = 0;
+        if (i < p.groups_per_xcd) {
+            b = fast_div(x + 8u * (uint32_t)i, p.div_hkv);
+            const int len = p.cu_q[b + 1] - p.cu_q[b];
+            spans = (uint32_t)(len + 127) >> 7;
+            n = spans * (uint32_t)p.items_per_span;
+        }
+        uint32_t incl = n;  // inclusive prefix sum over the lanes
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t t = (uint32_t)__shfl_up((int)incl, d);
+            if (lane >= d) incl += t;
+        }
+        const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+        if (k < base + total) {
+            const uint64_t hit = __builtin_amdgcn_ballot_w64(base + incl > k);
+            const int j = __builtin_ctzll(hit);
+            const uint32_t rem =
+                k - base - (__builtin_amdgcn_readlane(incl, j) - __builtin_amdgcn_readlane(n, j));
+            const uint32_t g = x + 8u * (uint32_t)(i0 + j);
+            const uint32_t bj = __builtin_amdgcn_readlane(b, j);
+            const uint32_t sj = __builtin_amdgcn_readlane(spans, j);
+            // inside the group: span from the top, head set, tile of the span
+            const uint32_t lo = rem & (uint32_t)(p.hp - 1), rest = rem >> p.hp_shift;
+            const uint32_t hi = fast_div(rest, p.div_group);
+            const int r = (int)(rest - hi * p.div_group.d);
+            const int qt_rev = (int)((hi << p.hp_shift) + lo);
+            it.b = (int)bj;
+            it.hkv = (int)(g - bj * p.div_hkv.d);
+            it.hq = it.hkv * p.group + (r << p.hp_shift);
+            it.qt = p.q_order ? qt_rev : (int)(sj << p.hp_shift) - 1 - qt_rev;
+            return it;
+        }
+        base += total;
+    }
+    return it;
+}
+
 __device__ __forceinline__ WorkItem decode_block(const AttnParams& p, int w)
 {
     // every divisor is launch-invariant: multiply-high and shift (fastdiv.h)
     WorkItem it;
     const uint32_t uw = (uint32_t)w;
     int qt_rev;
+    if (p.compact) return decode_packed(p, uw);
     if (p.map_mode == 1) {
         const uint32_t x = uw & 7, k = uw >> 3;
         const uint32_t c = fast_div(k, p.div_chunk_items);
@@ -393,14 +456,15 @@ __device__ __forceinline__ float final_score(float x, const AttnParams& p, const
 enum : int { kSideBoth = 0, kSideLeft = 1, kSideRight = 2 };
 
 // FOLD: this lane's additive constant of a tile's scores: the short soft-cap
-// form's C' (it ends in C' - 2C'/(1 + e)), minus the running max m_base, plus
-// the per-tile part of the position terms (ALiBi on one-sided tiles, the
-// relative position term always).
+// form's C' (it ends in C' - 2C'/(1 + e); not with POLY, whose polynomial
+// carries no constant), minus the running max m_base, plus the per-tile part
+// of the position terms (ALiBi on one-sided tiles, the relative position term
+// always).
 template <class T, int SIDE>
 __device__ __forceinline__ float fold_const(const WaveState<T>& ws, const AttnParams& p,
                                             const PosBase& pb, float m_base)
 {
-    float a = (T::CAP == kCapShort ? p.softcap_post_u : 0.0f) - m_base;
+    float a = (T::CAP == kCapShort && !T::POLY ? p.softcap_post_u : 0.0f) - m_base;
     if constexpr (T::BIAS == kBiasAlibi && SIDE == kSideLeft) a = __builtin_fmaf(ws.bias_abs, pb.abs, a);
     if constexpr (T::BIAS == kBiasAlibi && SIDE == kSideRight) a = __builtin_fmaf(-ws.bias_abs, pb.abs, a);
     if constexpr (T::BIAS == kBiasRelPos) a = __builtin_fmaf(ws.bias_lin, pb.lin, a);
@@ -408,13 +472,27 @@ __device__ __forceinline__ float fold_const(const WaveState<T>& ws, const AttnPa
 }
 
 // FOLD: the final score of element offset c minus the running max, from the
-// raw dot product and the tile constant a of fold_const.
-template <class T, int SIDE>
-__device__ __forceinline__ float fold_score(float dot, float a, const AttnParams& p,
+// raw dot product and the tile constant a of fold_const. With POLY the
+// soft-cap is C' tanh(y) = dot (b0 + z (b1 + z (b2 + z b3))), z = dot^2, an
+// odd polynomial valid while z <= cap_zmax (|y| <= 1/2; relative error below
+// 6e-7 there, the short form's order), four plain operations where the short
+// form takes two transcendental ones; EXACT (the fallback of a tile with a
+// larger |y|) takes the short form and adds the C' that a then lacks.
+template <class T, int SIDE, bool EXACT = false>
+__device__ __forceinline__ float fold_score(float dot, float z, float a, const AttnParams& p,
                                             const WaveState<T>& ws, const PosBase& pb, int c)
 {
     float u;
-    if constexpr (T::CAP == kCapShort) {
+    if constexpr (T::POLY && !EXACT) {
+        float q = __builtin_fmaf(z, p.cap_poly[3], p.cap_poly[2]);
+        q = __builtin_fmaf(z, q, p.cap_poly[1]);
+        q = __builtin_fmaf(z, q, p.cap_poly[0]);
+        u = __builtin_fmaf(dot, q, a);
+    } else if constexpr (T::POLY) {
+        const float e = __builtin_amdgcn_exp2f(dot * p.softcap_pre2);
+        u = __builtin_fmaf(-2.0f * p.softcap_post_u, __builtin_amdgcn_rcpf(1.0f + e),
+                           a + p.softcap_post_u);
+    } else if constexpr (T::CAP == kCapShort) {
         const float e = __builtin_amdgcn_exp2f(dot * p.softcap_pre2);
         u = __builtin_fmaf(-2.0f * p.softcap_post_u, __builtin_amdgcn_rcpf(1.0f + e), a);
     } else if constexpr (T::CAP == kCapExact) {
@@ -685,6 +763,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     s16x4 vlo[PV], vhi[PV];
     RowSums rs = {0.0f, 0.0f};
     float mx = -__builtin_inff();
+    float zmax = 0.0f;  // POLY: the largest dot^2 of the next tile
 
     auto read_k = [&](int i) __attribute__((always_inline)) {
         const int b = i / T::KSTEPS, t = i % T::KSTEPS;
@@ -744,8 +823,16 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             // element (bb, e) is key jn + 8lh + c, c = 32bb + e + (e >= 8 ? 8 : 0)
             constexpr int c = 32 * bb + e + (e >= 8 ? 8 : 0);
             float x = sn[bb][e];
-            if constexpr (T::FOLD)
-                x = fold_score<T, SIDE>(x, fa, p, ws, pb, c);
+            if constexpr (T::POLY) {
+                const float z = x * x;
+                zmax = __builtin_fmaxf(zmax, z);
+                x = fold_score<T, SIDE>(x, z, fa, p, ws, pb, c);
+                // keep the score's arithmetic in this slice: the fallback below
+                // overwrites it, so the compiler would otherwise sink it past
+                // the products into the common path's successor
+                asm volatile("" : "+v"(x));
+            } else if constexpr (T::FOLD)
+                x = fold_score<T, SIDE>(x, 0.0f, fa, p, ws, pb, c);
             else if constexpr (T::MODS)
                 x = final_score<T>(x, p, ws, pb, c);
             if constexpr (MASKED)
@@ -759,6 +846,25 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
         mx = pair_max(mx);
         if constexpr (!T::MODS) mx *= p.scale_u;  // raw max -> log2 units (scale > 0)
         update_max(ws, mx);
+    }
+    if constexpr (T::POLY) {
+        // Rare: a score of the tile lies beyond the polynomial's range. K of
+        // the tile is still in LDS (the next step's loads fill the other
+        // buffer), so the wave recomputes its dot products and takes the
+        // short form for the whole tile.
+        if (__builtin_amdgcn_ballot_w64(zmax > p.cap_zmax)) {
+            qk_tile<T>(kread, ws, sn);
+#pragma unroll
+            for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int c = 32 * bb + e + (e >= 8 ? 8 : 0);
+                    float x = fold_score<T, SIDE, true>(sn[bb][e], 0.0f, fa, p, ws, pb, c);
+                    if constexpr (MASKED)
+                        if (!visible<T>(mt, c)) x = -__builtin_inff();
+                    sn[bb][e] = x;
+                }
+        }
     }
 }
 
@@ -939,7 +1045,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     // Read the kernel arguments the set-up needs in one round of scalar loads
     // (the branches below would otherwise spread them over several).
     __builtin_amdgcn_sched_barrier(0);
-    asm volatile("" ::"s"(p.map_mode), "s"(p.hp_shift), "s"(p.num_q_tiles), "s"(p.q_order),
+    asm volatile("" ::"s"(p.compact), "s"(p.map_mode), "s"(p.hp_shift), "s"(p.num_q_tiles), "s"(p.q_order),
                  "s"(p.div_bh.mul), "s"(p.div_bh.shift), "s"(p.div_bh.d), "s"(p.div_hq.mul),
                  "s"(p.div_hq.shift), "s"(p.div_hq.d), "s"(p.div_group.mul),
                  "s"(p.div_group.shift), "s"(p.div_group.d), "s"(p.div_hkv.mul),
@@ -960,7 +1066,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         lk = p.seqlen_k;
     }
     const int q0 = it.qt * p.wg_rows;
-    if (q0 >= lq) return;  // whole workgroup: tile past this sequence's end
+    if (it.qt < 0 || q0 >= lq) return;  // whole workgroup: no item, or past the sequence's end
     const int hkv = it.hkv;
     // Wave w takes query head hq + (w mod hp) and the 32-row block w / hp of
     // the workgroup's rows (hp = 1: four row blocks of one head; hp = 4: the
@@ -1018,6 +1124,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
                                   (dd & 7) * 2;
             }
     }
+
     const uint32_t klp = load_lane_offset<T>(wave, lane, p.sk_s);
     const uint32_t vlp = load_lane_offset<T>(wave, lane, p.sv_s);
     // One buffer descriptor per K/V slice; its range ends at the sequence end.
@@ -1328,8 +1435,7 @@ template <int D, int CAP, int BIAS, int NORM, bool GEN, bool LEFT = true, bool G
 hipError_t launch_variant(const AttnParams& p, hipStream_t stream)
 {
     using T = Traits<D, key_tile_width(D), CAP, BIAS, NORM, GEN, LEFT, GLIST>;
-    int64_t blocks = (int64_t)p.num_q_tiles * (p.hq >> p.hp_shift) * p.batch;
-    hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)blocks), dim3(NT), 0, stream, p);
+    hipLaunchKernelGGL((attn_fwd_bf16_kernel<T>), dim3((unsigned)p.grid), dim3(NT), 0, stream, p);
     return hipGetLastError();
 }
 
@@ -1339,7 +1445,10 @@ template <class F>
 hipError_t with_cap(const AttnParams& p, F&& f)
 {
     if (p.softcap <= 0.0f) return f(std::integral_constant<int, kCapOff>{});
-    if (p.softcap <= kCapShortMax) return f(std::integral_constant<int, kCapShort>{});
+    // (the short form's kernels that fold the running max take the soft-cap
+    // from a polynomial whose coefficients must be normal floats)
+    if (p.softcap <= kCapShortMax && p.cap_zmax >= 0.0f)
+        return f(std::integral_constant<int, kCapShort>{});
     return f(std::integral_constant<int, kCapExact>{});
 }
 

@@ -31,6 +31,12 @@ struct AttnParams {
     int32_t map_mode;        // workgroup order (0 natural, 1 kv-group per XCD)
     int32_t q_order;         // query tiles issued 0 last-first (causal-like), 1 first-first
     int32_t chunk;           // map_mode 1: kv-head groups per chunk within an XCD
+    // bf16 variable-length batches with map_mode 1 and chunk 1: the grid holds
+    // only the query spans (128 rows) of each sequence (decode_packed)
+    int32_t compact;
+    int32_t groups_per_xcd;  // batch * hkv / 8
+    int32_t items_per_span;  // workgroups per 128-row span of a kv group: group / hp * hp
+    int32_t grid;            // bf16: workgroups launched
     // The divisors of the workgroup-id decode, prepared for fast_div.
     // A head set is the hp query heads of one workgroup; a kv group holds
     // group / hp of them.
@@ -68,4 +74,9 @@ struct AttnParams {
     float softcap_pre;       // scale / C
     float softcap_pre2;      // 2 log2(e) scale / C
     float softcap_post_u;    // C * unit
+    // Soft-cap as an odd polynomial in the raw dot product (kCapShort kernels
+    // that fold the running max): C' tanh(scale * dot / C) =
+    // dot * sum_k cap_poly[k] dot^(2k) while dot^2 <= cap_zmax.
+    float cap_poly[4];
+    float cap_zmax;
 };

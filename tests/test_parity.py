@@ -17,6 +17,7 @@ from gpu_util import assert_parity, gpu_available, log, run_gpu, sample_rows
 from paper_2605_05023_amd import ATTN_MASK_CAUSAL as CAUSAL
 from paper_2605_05023_amd import ATTN_MASK_NONE as NONE
 from paper_2605_05023_amd import ATTN_MASK_SLIDING_WINDOW as WINDOW
+from paper_2605_05023_amd import ATTN_MASK_GLOBAL_SLIDING_WINDOW as MASK_GLOBAL_WINDOW
 from paper_2605_05023_amd import fwd
 from paper_2605_05023_amd.workloads import WORKLOAD_ORDER, WORKLOADS, Workload, make_inputs
 
@@ -106,6 +107,34 @@ RAMPS = [
     ("bf16_d128_softcap_up", "bf16", 128, CAUSAL, -1, -1, 1e4, 150.0),
     ("fp32_d64_causal_up", "fp32", 64, CAUSAL, -1, -1, 0.0, 150.0),
 ]
+
+
+# Soft-cap kernels that fold the running max take C tanh(s / C) from an odd
+# polynomial while every |s / C| of a tile stays within 1/2, and recompute a
+# tile with the closed form otherwise. Key rows 64..127 are scaled up so that
+# their tiles leave the polynomial's range while the other tiles stay inside
+# it: both forms run in one launch, on neighbouring tiles of the same rows.
+CAP_RANGE = [
+    ("bf16_d64_alibi_softcap30", 64, NONE, dict(alibi=True, softcap=30.0, sigma=1.5)),
+    ("bf16_d128_causal_softcap30", 128, CAUSAL, dict(softcap=30.0)),
+    ("bf16_d128_causal_relpos_softcap20", 128, CAUSAL, dict(softcap=20.0, relpos=True)),
+]
+
+
+@pytest.mark.parametrize("case", CAP_RANGE, ids=[c[0] for c in CAP_RANGE])
+def test_softcap_polynomial_range(case):
+    name, D, mask, kw = case
+    log(f"[parity soft-cap range] {name}")
+    wl = dataclasses.replace(W(name, "bf16", 1, 2, 2, 300, D, mask, seed=23), **kw)
+    inp = make_inputs(wl)
+    k = inp.k.float()
+    k[..., 64:128, :] *= 6.0
+    inp = dataclasses.replace(inp, k=k.to(torch.bfloat16))
+    y = (inp.q.float() @ inp.k.float().transpose(-1, -2)).abs() * wl.scale / wl.softcap
+    assert float(y[..., :64].max()) < 0.5 and float(y[..., 64:128].max()) > 0.5
+    o, lse = run_gpu(inp)
+    torch.cuda.synchronize()
+    assert_parity(inp, o, lse, label=name)
 
 
 @pytest.mark.parametrize("case", RAMPS, ids=[c[0] for c in RAMPS])
@@ -271,6 +300,54 @@ def test_chunked_order_forced(chunk):
         log(f"[chunked] {wl.name} chunk={chunk}")
         o, lse = run_gpu(inp, order="xcd_groups", chunk=chunk)
         assert_parity(inp, o, lse, label=f"{wl.name} chunk {chunk}")
+
+
+# Packed variable-length grid: with the kv groups of each XCD walked one at a
+# time (the packed workload's schedule, forced here through the overrides),
+# the grid holds only the 128-row query spans each sequence has, and every
+# workgroup finds its sequence from prefix sums over the XCD's groups, 64
+# groups at a time. Cases: group sizes 4, 1 and 2 (all heads-per-workgroup
+# choices), two kv heads of one sequence on one XCD (Hkv = 16), empty and
+# one-token sequences, more than 64 groups per XCD (130 sequences x 8 kv
+# heads), and the ascending tile order of the global sliding window. Each
+# case has lengths skewed enough that the packed grid is the smaller one.
+PACKED = [
+    ("gqa4_causal", 8, 2, 128, dict(mask=CAUSAL), [1, 0, 130, 64, 1000, 5, 300, 128]),
+    ("mha_hkv16_causal", 16, 16, 64, dict(mask=CAUSAL), [700, 5]),
+    ("gqa2_window", 16, 8, 128, dict(mask=WINDOW, window_left=40, window_right=0),
+     [129, 0, 77]),
+    ("many_groups", 8, 8, 64, dict(mask=CAUSAL), "many"),
+    ("global_window", 4, 1, 128, dict(mask=MASK_GLOBAL_WINDOW, window_left=16,
+                                      window_right=16, num_global=3),
+     [70, 1000, 0, 1, 130, 64, 33, 256] + [40] * 16),
+]
+
+
+def packed_grid_applies(lengths, hq, hkv):
+    """The library's rule for taking the packed grid (bf16, map mode 1, chunk 1)."""
+    group = hq // hkv
+    hp = 4 if group % 4 == 0 else 2 if group % 2 == 0 else 1
+    B, gsets = len(lengths), group // hp
+    spans = -(-max(lengths) // 128)
+    padded = spans * hp * (hq // hp) * B
+    packed = 8 * (-(-hkv // 8) * sum(lengths) // 128 + B * hkv // 8) * gsets * hp
+    return packed < padded
+
+
+@pytest.mark.parametrize("case", PACKED, ids=[c[0] for c in PACKED])
+def test_varlen_packed_grid(case):
+    name, hq, hkv, D, kw, lengths = case
+    if lengths == "many":
+        g = torch.Generator().manual_seed(9)
+        lengths = torch.randint(0, 300, (130,), generator=g).tolist()
+        lengths[7], lengths[8] = 0, 500
+    assert packed_grid_applies(lengths, hq, hkv)
+    log(f"[parity packed grid] {name} B={len(lengths)}")
+    wl = Workload(name, "bf16", len(lengths), hq, hkv, 0, D, seed=27, varlen=True, **kw)
+    inp = make_inputs(wl, lengths=lengths)
+    o, lse = run_gpu(inp, order="xcd_groups", chunk=1)
+    torch.cuda.synchronize()
+    assert_parity(inp, o, lse, label=name)
 
 
 @pytest.mark.parametrize("hp,order", [(1, "natural"), (2, "natural"), (4, "natural"),
