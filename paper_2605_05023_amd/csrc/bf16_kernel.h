@@ -632,7 +632,7 @@ template <class T, bool SHIFT = true>
 __device__ __forceinline__ RowSums exp_tile(const f32x16 (&s)[T::NB], u32x4 (&pw)[T::NB][2],
                                             float m_use, float scale_u)
 {
-    RowSums rs = {0.0f, 0.0f};
+    RowSums rs = {-0.0f, -0.0f};  // -0 + x == x for every x: the first add folds away
 #pragma unroll
     for (int b = 0; b < T::NB; ++b) {
 #pragma unroll
@@ -671,7 +671,7 @@ __device__ __forceinline__ void check_tile(WaveState<T>& ws, const f32x16 (&s)[T
     if constexpr (!T::SOFTMAX) return;
     if constexpr (!T::MAXFREE) {
         ws.l_run += rs.f;
-        ws.l_o += rs.b;
+        if constexpr (T::PSUM_BF16) ws.l_o += rs.b;
         return;
     }
     bool need = rs.f > PSUM_BOUND;
@@ -703,7 +703,7 @@ __device__ __forceinline__ void check_tile(WaveState<T>& ws, const f32x16 (&s)[T
                                p.scale_u);
     }
     ws.l_run += rs.f;
-    ws.l_o += rs.b;
+    if constexpr (T::PSUM_BF16) ws.l_o += rs.b;
 }
 
 // O^T += V^T P^T for the V tile in LDS at `vt`.
@@ -761,7 +761,7 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     u32x4 pw[NB][2];
     bf16x8 kop[QK];
     s16x4 vlo[PV], vhi[PV];
-    RowSums rs = {0.0f, 0.0f};
+    RowSums rs = {-0.0f, -0.0f};  // -0 + x == x for every x: the first add folds away
     float mx = -__builtin_inff();
     float zmax = 0.0f;  // POLY: the largest dot^2 of the next tile
 
