@@ -794,6 +794,11 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
             const float p0 = norm_value<T, !T::FOLD>(sc[bb][e], m_use, p.scale_u);
             const float p1 = norm_value<T, !T::FOLD>(sc[bb][e + 1], m_use, p.scale_u);
             pw[bb][e / 8][(e % 8) / 2] = pack_bf16(p0, p1);
+            // MAXFREE: keep the conversion in this slice. check_tile may
+            // recompute P, so the compiler would otherwise sink it past the
+            // check, where it runs unhidden before the first P V product and
+            // keeps the fp32 P alive across the branch.
+            if constexpr (T::MAXFREE) asm volatile("" : "+v"(pw[bb][e / 8][(e % 8) / 2]));
             if constexpr (T::SOFTMAX) {
                 rs.f += p0;
                 rs.f += p1;
