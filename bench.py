@@ -1,6 +1,6 @@
 """Benchmark of the fused attention forward on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload varlen_gqa_bf16]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--also A,B]
 
 A step is one attn_fwd call (the whole fused forward) over one batch of the
 seeded synthetic workload, with inputs already resident in HBM. The default
@@ -10,7 +10,11 @@ dimension 128. Prints one
 JSON line: throughput in TFLOP/s counting only unmasked score entries
 (4 * head_dim FLOPs per visible query/key pair per query head), the roofline
 of the kernel against the bf16 matrix-core peak, and the CPU oracle timed on a
-bounded sample of the same workload on the host cores.
+bounded sample of the same workload on the host cores. Without --workload the
+line also carries `other_configs`: the other four headline workloads (fp32
+plain, causal, GQA sliding window, ALiBi + soft-cap), each timed after the
+reported one with the same warm-up and step counts; `value` stays that of the
+default workload.
 """
 from __future__ import annotations
 
@@ -199,12 +203,72 @@ def row_flops_fn(inp):
     return fn
 
 
+DEFAULT_WORKLOAD = "varlen_gqa_bf16"
+# the workloads the metric is quoted on: fp32 plain, causal, GQA window,
+# ALiBi + soft-cap, packed variable-length causal GQA
+HEADLINE = ("plain_fp32", "causal_bf16", "gqa_swa_bf16", "alibi_softcap_bf16", "varlen_gqa_bf16")
+
+
+def time_other(name: str, steps: int, warmup: int, dev) -> dict:
+    """One further workload, timed like the reported one: `warmup` launches,
+    then `steps` launches between HIP events on the launching stream and the
+    host clock. Its inputs are freed afterwards."""
+    wl = WORKLOADS[name]
+    inp = make_inputs(wl)
+    q, k, v = inp.q.to(dev), inp.k.to(dev), inp.v.to(dev)
+    out = torch.empty_like(q)
+    varlen = inp.cu_seqlens is not None
+    lse_shape = (wl.hq, inp.total_tokens) if varlen else (wl.batch, wl.hq, wl.seqlen)
+    lse = torch.empty(lse_shape, dtype=torch.float32, device=dev) if wl.norm == "softmax" else None
+    vkw = inp.variant_kwargs(dev)
+    stream = torch.cuda.current_stream(dev)
+    desc = attn.make_desc(q, k, v, out, stream=stream.cuda_stream, **vkw)
+    lib = attn.load()
+    args_c = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+              lse.data_ptr() if lse is not None else None, ctypes.byref(desc))
+    for _ in range(warmup):
+        attn.check(lib.attn_fwd(*args_c), lib)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        attn.check(lib.attn_fwd(*args_c), lib)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = e0.elapsed_time(e1) / steps
+    flops = 4 * wl.head_dim * visible_pairs(inp)
+    ms_per_step = wall * 1e3 / steps
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    achieved = flops / (kernel_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    return {
+        "workload": name,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "value": round(value, 2),
+        "ms_per_step": round(ms_per_step, 5),
+        "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "kernel_avg_ms": round(kernel_ms, 5),
+        "achieved": round(achieved, 2),
+        "peak": peak,
+        "frac": round(achieved / peak, 4),
+        "unmasked_flops_per_step": flops,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="varlen_gqa_bf16", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default=None, choices=sorted(WORKLOADS),
+                    help="workload of the reported value (default varlen_gqa_bf16)")
+    ap.add_argument("--also", default=None,
+                    help="comma-separated further workloads timed after the reported one, in the "
+                         "same way, into other_configs (default: the other headline workloads "
+                         "when --workload is not given, none otherwise; 'none' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="minimum oracle time for the CPU baseline sample")
@@ -219,6 +283,17 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
+
+    also = args.also
+    if args.workload is None:
+        args.workload = DEFAULT_WORKLOAD
+        if also is None:
+            also = ",".join(w for w in HEADLINE if w != DEFAULT_WORKLOAD)
+    also = [] if also in (None, "", "none") else also.split(",")
+    for w in also:
+        if w not in WORKLOADS:
+            print(f"bench.py: unknown workload {w} in --also", file=sys.stderr)
+            sys.exit(2)
 
     dev = torch.device("cuda:0")
     wl = WORKLOADS[args.workload]
@@ -344,6 +419,9 @@ def main():
             "algorithmic_gbps": round(nbytes / (kernel_ms * 1e-3) / 1e9, 1),
         },
     }
+    if also:
+        del q, k, v, out, lse, vkw, desc
+        result["other_configs"] = [time_other(w, args.steps, args.warmup, dev) for w in also]
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(inp, row_flops_fn(inp), args.cpu_seconds,
                                               4 * args.cpu_seconds, seed=wl.seed)
