@@ -475,6 +475,15 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     const bool glist = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.global_tokens &&
                        d.num_global > 0;
     p.gtok = glist ? d.global_tokens : nullptr;
+    p.glob_items = 0;
+    p.glob_chunks = 1;
+    if (glist && d.dtype == ATTN_BF16) {
+        p.glob_chunks = (int32_t)((d.num_global + block_m - 1) / block_m);
+        const int64_t items = (int64_t)d.batch * hsets * p.glob_chunks;
+        if ((int64_t)p.grid + items > INT32_MAX) return ATTN_ERR_UNSUPPORTED;
+        p.glob_items = (int32_t)items;
+        p.grid += p.glob_items;
+    }
     if (d.flags & ATTN_FLAG_VALIDATE) {
         rc = validate_device_inputs(d, varlen, segment_mask(d.mask_kind), glist);
         if (rc != ATTN_OK) return rc;

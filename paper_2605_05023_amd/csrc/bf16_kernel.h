@@ -1058,7 +1058,29 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
                  "s"(p.seqlen_k), "s"(p.wg_rows), "s"(p.q), "s"(p.k), "s"(p.v), "s"(p.o),
                  "s"(p.sq_b), "s"(p.sq_h), "s"(p.sq_s), "s"(p.sk_b), "s"(p.sk_h), "s"(p.sk_s),
                  "s"(p.sv_b), "s"(p.sv_h), "s"(p.sv_s), "s"(p.so_h), "s"(p.so_s));
-    const WorkItem it = decode_block(p, blockIdx.x);
+    // Listed global set: the first glob_items workgroups compute the rows
+    // whose position is in G (every key visible), wg_rows list entries each,
+    // for one head set of one sequence; the others are the ordinary work
+    // items, whose rows in G are left to them. Rows that see every key then
+    // no longer stretch an ordinary workgroup over the whole key range.
+    bool gmode = false;
+    WorkItem it;
+    if constexpr (T::GLIST) {
+        gmode = (int)blockIdx.x < p.glob_items;
+        if (gmode) {
+            const int e = (int)blockIdx.x;
+            const int hsets = p.hq >> p.hp_shift;
+            const int c = e % p.glob_chunks, bh = e / p.glob_chunks;
+            it.b = bh / hsets;
+            it.hq = (bh - it.b * hsets) << p.hp_shift;
+            it.hkv = it.hq / p.group;
+            it.qt = c;  // chunk of the list
+        } else {
+            it = decode_block(p, (int)blockIdx.x - p.glob_items);
+        }
+    } else {
+        it = decode_block(p, blockIdx.x);
+    }
     int lq, lk;
     int64_t qrow0 = 0, krow0 = 0;  // first token of the sequence (varlen)
     if (p.cu_q) {
@@ -1070,7 +1092,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
         lq = p.seqlen_q;
         lk = p.seqlen_k;
     }
-    const int q0 = it.qt * p.wg_rows;
+    const int q0 = gmode ? 0 : it.qt * p.wg_rows;
     if (it.qt < 0 || q0 >= lq) return;  // whole workgroup: no item, or past the sequence's end
     const int hkv = it.hkv;
     // Wave w takes query head hq + (w mod hp) and the 32-row block w / hp of
@@ -1100,8 +1122,18 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
 
     WaveState<T> ws;
     ws.lh = lh;
-    // Q fragment: lane holds row q0 + 32*rblk + li, dims 16t + 8lh .. +7.
-    const int qi = q0 + rblk * 32 + li;
+    // Q fragment: lane holds row q0 + 32*rblk + li (a global row: the row at
+    // list entry wg_rows * chunk + 32*rblk + li), dims 16t + 8lh .. +7.
+    int qi = q0 + rblk * 32 + li;
+    bool row_ok = qi < lq;  // the row exists and this workgroup writes it
+    if constexpr (T::GLIST) {
+        if (gmode) {
+            const int k = it.qt * p.wg_rows + rblk * 32 + li;
+            qi = k < p.num_global ? p.gtok[k] - (lk - lq) : -1;
+            row_ok = qi >= 0 && qi < lq;
+            if (!row_ok) qi = 0;  // (its Q load stays in range; nothing is written)
+        }
+    }
     {
         uint32_t bytes = (uint32_t)((((int64_t)lq - 1) * p.sq_s + D) * 2);
         __amdgpu_buffer_rsrc_t qrs = make_rsrc(qb + qoff, bytes);
@@ -1167,17 +1199,24 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             __syncthreads();
         }
         RowVis rv = {0, 1, 0};
-        if (qi < lq) {
-            if constexpr (T::GLIST)
-                rv = row_vis_listed(p.band, gl, ng, qi, lq, lk);
-            else
+        if (row_ok) {
+            if constexpr (T::GLIST) {
+                if (gmode) {
+                    rv.jlo = 0;
+                    rv.jhi = lk - 1;
+                } else if (listed(gl, ng, qi + (lk - lq))) {
+                    row_ok = false;  // a row of G: the global-row items write it
+                } else {
+                    rv = row_vis_listed(p.band, gl, ng, qi, lq, lk);
+                }
+            } else
                 rv = row_visibility(p.mask_kind, p.band, p.num_global, seg, p.num_seg,
                                     p.query_start, qi, lq, lk);
         }
         ws.pfx = rv.pfx;
         ws.jlo = rv.jlo;
         ws.jhi = rv.jhi;
-        tr = plan_general<BN>(rv, qi < lq, red, wave, lane);
+        tr = plan_general<BN>(rv, row_ok, red, wave, lane);
         jbeg = 0;
         jend = tr.n;
     } else {
@@ -1387,7 +1426,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
             last_step<T>(lds_v0, ws, ws.sa, p, m_use, tile_of(j) * BN);
     }
     if constexpr (T::GLIST)
-        gathered_tiles<T>(ws, p, gl, ng, lds_k0, lds_v0, krs, vrs, krow, vrow, lk, qi < lq, wave,
+        if (!gmode)  // (global rows see every key through the planned tiles)
+            gathered_tiles<T>(ws, p, gl, ng, lds_k0, lds_v0, krs, vrs, krow, vrow, lk, row_ok, wave,
                           lane);
 
     // Epilogue. Softmax: O = O^T / l (with PSUM_BF16 the sum of the bf16 P
@@ -1403,7 +1443,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     } else {
         inv = lk > 0 ? 1.0f / (float)lk : 0.0f;
     }
-    if (qi < lq) {
+    if (row_ok) {
         __bf16* orow = ob + ooff + (int64_t)qi * p.so_s;
 #pragma unroll
         for (int d = 0; d < T::DBLK; ++d) {

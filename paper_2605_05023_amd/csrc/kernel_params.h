@@ -37,6 +37,9 @@ struct AttnParams {
     int32_t groups_per_xcd;  // batch * hkv / 8
     int32_t items_per_span;  // workgroups per 128-row span of a kv group: group / hp * hp
     int32_t grid;            // bf16: workgroups launched
+    // bf16 listed global set: the first glob_items workgroups compute the rows
+    // of G, wg_rows list entries each (glob_chunks per sequence and head set)
+    int32_t glob_items, glob_chunks;
     // The divisors of the workgroup-id decode, prepared for fast_div.
     // A head set is the hp query heads of one workgroup; a kv group holds
     // group / hp of them.

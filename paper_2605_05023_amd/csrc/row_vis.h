@@ -97,6 +97,13 @@ ATTN_HD RowVis row_visibility(int32_t kind, KeyBand band, int32_t num_global, co
 // Is key j visible under `r`?
 ATTN_HD bool row_sees(RowVis r, int32_t j) { return j < r.pfx || (j >= r.jlo && j <= r.jhi); }
 
+// Is key-axis position ip one of the sorted list g of ng positions?
+ATTN_HD bool listed(const int32_t* g, int32_t ng, int32_t ip)
+{
+    const int32_t k = ip >= 0 ? segment_of(g, ng, ip) : -1;
+    return k >= 0 && g[k] == ip;
+}
+
 // Global sliding window with G given as a sorted list g of ng positions: a row
 // whose key-axis position is in G sees every key; any other row sees its
 // window band here, and the keys of G outside that band are taken separately

@@ -11,6 +11,7 @@ variant's edges (4096 seeded rows of the 524,288: the oracle takes a minute
 per workload for all of them). Bars: softmax O max-abs 2e-2 (bf16) / 1e-4 (fp32) and LSE
 1e-3; ReLU / Sigmoid O within that fraction of max|O_ref| (no LSE).
 """
+import numpy as np
 import pytest
 
 from gpu_util import assert_parity, gpu_available, log, run_gpu, sample_rows
@@ -75,6 +76,10 @@ SMALL = [
       window_right=0, global_list=(3, 64, 65, 200, 330, 500)),
     W("glist_d128_run_of_70", "bf16", 1, 4, 4, 400, 128, MASK_GLOBAL_WINDOW, window_left=8,
       window_right=8, global_list=tuple(range(100, 170)) + (399,)),
+    # grouped heads (32 rows per workgroup): 70 global rows take three chunks of
+    # the list, the last one partial, and a position past the end is ignored
+    W("glist_d128_gqa4_three_chunks", "bf16", 2, 8, 2, 300, 128, MASK_GLOBAL_WINDOW,
+      window_left=12, window_right=3, global_list=tuple(range(5, 285, 4)) + (299, 400)),
     W("glist_d128_single_w0", "bf16", 1, 2, 2, 200, 128, MASK_GLOBAL_WINDOW, window_left=0,
       window_right=0, global_list=(77,)),
     W("glist_d64_alibi_relpos_softcap", "bf16", 1, 4, 4, 260, 64, MASK_GLOBAL_WINDOW,
@@ -159,6 +164,12 @@ def test_varlen_next(wl):
 def test_full_next(name):
     inp = make_inputs(WORKLOADS[name])
     rows = sample_rows(inp, 4096, seed=3)
+    wl = inp.wl
+    if wl.global_list:  # every row of the listed global set, in every head
+        S = wl.seqlen
+        g = [x for x in wl.global_list if x < S]
+        extra = [(b * wl.hq + h) * S + x for b in range(wl.batch) for h in range(wl.hq) for x in g]
+        rows = np.unique(np.concatenate([np.asarray(rows, dtype=np.int64), extra]))
     log(f"[next full] {name}: {len(rows)} sampled rows")
     o, lse = run_gpu(inp)
     assert_parity(inp, o, lse, rows=rows, label=name)
