@@ -14,6 +14,7 @@
 #include "kernel_params.h"
 #include "launch.h"
 #include "row_vis.h"
+#include "softcap_poly.h"
 
 namespace {
 
@@ -373,22 +374,26 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.softcap_pre2 = p.softcap_pre * (float)(2.0 * 1.4426950408889634);
     p.softcap_post_u = d.softcap * p.unit;
     {
-        // tanh(y) / y ~= a0 + a1 y^2 + a2 y^4 + a3 y^6 on |y| <= 1/2: Remez
-        // fit of the relative error (max 5.5e-7) in y^2 over [0, 1/4]. With
-        // s = scale / C the soft-cap is C' tanh(s dot) = dot sum_k b_k dot^(2k),
-        // b_k = C' s^(2k+1) a_k, valid while dot^2 <= (1 / (2 s))^2.
-        static const double a[4] = {0.99999946, -0.33326318, 0.13190297, -0.04440223};
+        // Soft-cap as dot (b0 + z (b1 + z b2)), z = dot^2 (softcap_poly.h):
+        // the widest tabulated range |y| <= R, y = (scale / C) dot, whose
+        // error bound C' R rel stays within kCapPolyMaxErr; the polynomial
+        // holds while dot^2 <= (R / s)^2.
         p.cap_zmax = -1.0f;  // no polynomial (kernels take the exact form)
         if (d.softcap > 0.0f) {
             const double sc = (double)d.scale / d.softcap, cu = (double)p.softcap_post_u;
-            bool normal = true;
+            int f = 0;
+            while (f + 1 < kCapPolyFitCount &&
+                   cu * kCapPolyFits[f].r * kCapPolyFits[f].rel > kCapPolyMaxErr)
+                ++f;
+            const CapPolyFit& fit = kCapPolyFits[f];
+            bool normal = cu * fit.r * fit.rel <= kCapPolyMaxErr;
             double sk = sc;
-            for (int k = 0; k < 4; ++k) {
-                p.cap_poly[k] = (float)(cu * sk * a[k]);
+            for (int k = 0; k < 3; ++k) {
+                p.cap_poly[k] = (float)(cu * sk * fit.a[k]);
                 normal = normal && std::fabs(p.cap_poly[k]) >= 1.1754943508222875e-38;
                 sk *= sc * sc;
             }
-            const double zmax = 0.25 / (sc * sc);
+            const double zmax = (double)fit.r * fit.r / (sc * sc);
             if (normal) p.cap_zmax = zmax < 3.0e38 ? (float)zmax : 3.0e38f;
         }
     }

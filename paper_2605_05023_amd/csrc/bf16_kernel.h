@@ -473,19 +473,19 @@ __device__ __forceinline__ float fold_const(const WaveState<T>& ws, const AttnPa
 
 // FOLD: the final score of element offset c minus the running max, from the
 // raw dot product and the tile constant a of fold_const. With POLY the
-// soft-cap is C' tanh(y) = dot (b0 + z (b1 + z (b2 + z b3))), z = dot^2, an
-// odd polynomial valid while z <= cap_zmax (|y| <= 1/2; relative error below
-// 6e-7 there, the short form's order), four plain operations where the short
-// form takes two transcendental ones; EXACT (the fallback of a tile with a
-// larger |y|) takes the short form and adds the C' that a then lacks.
+// soft-cap is C' tanh(y) = dot (b0 + z (b1 + z b2)), z = dot^2, an odd
+// polynomial valid while z <= cap_zmax (|y| <= R, the range the host chose
+// for C so that the score errs by at most 1e-4 units; softcap_poly.h), three
+// plain operations where the short form takes two transcendental ones; EXACT
+// (the fallback of a tile with a larger |y|) takes the short form and adds
+// the C' that a then lacks.
 template <class T, int SIDE, bool EXACT = false>
 __device__ __forceinline__ float fold_score(float dot, float z, float a, const AttnParams& p,
                                             const WaveState<T>& ws, const PosBase& pb, int c)
 {
     float u;
     if constexpr (T::POLY && !EXACT) {
-        float q = __builtin_fmaf(z, p.cap_poly[3], p.cap_poly[2]);
-        q = __builtin_fmaf(z, q, p.cap_poly[1]);
+        float q = __builtin_fmaf(z, p.cap_poly[2], p.cap_poly[1]);
         q = __builtin_fmaf(z, q, p.cap_poly[0]);
         u = __builtin_fmaf(dot, q, a);
     } else if constexpr (T::POLY) {

@@ -78,8 +78,8 @@ struct AttnParams {
     float softcap_pre2;      // 2 log2(e) scale / C
     float softcap_post_u;    // C * unit
     // Soft-cap as an odd polynomial in the raw dot product (kCapShort kernels
-    // that fold the running max): C' tanh(scale * dot / C) =
+    // that fold the running max; softcap_poly.h): C' tanh(scale * dot / C) =
     // dot * sum_k cap_poly[k] dot^(2k) while dot^2 <= cap_zmax.
-    float cap_poly[4];
+    float cap_poly[3];
     float cap_zmax;
 };
