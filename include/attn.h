@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define ATTN_ABI_VERSION 3
+#define ATTN_ABI_VERSION 4
 
 /* Largest attn_variant_desc.num_segments, and num_global when global_tokens
  * lists the global positions (both are staged on chip). */
@@ -204,6 +204,16 @@ typedef struct attn_variant_desc {
     int32_t sched_chunk;         /* with sched_order 2 (or the library choosing
                                     it): kv groups walked per chunk within an XCD,
                                     1 .. batch * Hkv / 8                          */
+    /* Per-sequence index-mask layouts. 0: one segment_starts (global_tokens)
+       array serves every sequence. Otherwise sequence s (batch entry, or packed
+       sequence when varlen) reads its own num_segments (num_global) entries at
+       segment_starts + s * segment_stride (global_tokens + s * global_stride),
+       each array with the rules above; stride >= the entry count. A sequence
+       with fewer segments or global positions pads its array with strictly
+       increasing positions at or past its end (empty segments, ignored
+       global positions). */
+    int64_t segment_stride;      /* SHARE_QUESTION, CAUSAL_BLOCKWISE              */
+    int64_t global_stride;       /* GLOBAL_SLIDING_WINDOW with global_tokens       */
 } attn_variant_desc;
 
 /*

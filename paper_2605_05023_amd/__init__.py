@@ -46,6 +46,22 @@ def _int_array(t, name, device):
         raise ValueError(f"{name} must be one-dimensional")
 
 
+def _layout_array(t, name, device, nseq):
+    """An index-mask layout: one int32 array shared by every sequence, or one
+    row per sequence ([nseq, n], rows contiguous). Returns (entries, stride)."""
+    if t.dtype != torch.int32 or t.device != device:
+        raise TypeError(f"{name} must be int32 on q's device")
+    if t.dim() == 1:
+        if not t.is_contiguous():
+            raise TypeError(f"{name} must be contiguous")
+        return t.numel(), 0
+    if t.dim() != 2 or t.shape[0] != nseq:
+        raise ValueError(f"{name} must be [n] or [{nseq} sequences, n], got {tuple(t.shape)}")
+    if t.shape[1] > 0 and (t.stride(1) != 1 or t.stride(0) < t.shape[1]):
+        raise ValueError(f"{name} rows must be contiguous and not overlap")
+    return t.shape[1], t.stride(0) if t.shape[1] > 0 else 0
+
+
 def lse_shape(q, varlen: bool):
     """Shape of the fp32 LSE output for q: (B, Hq, Sq), or (Hq, Tq) when varlen."""
     return (q.shape[1], q.shape[0]) if varlen else (q.shape[0], q.shape[1], q.shape[2])
@@ -91,6 +107,8 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
     `window` gives the (left, right) bounds of the two window masks;
     `global_tokens` (device int32, strictly increasing) lists the global
     positions of the global sliding window (else positions 0..num_global-1).
+    `segment_starts` and `global_tokens` are one array shared by every
+    sequence, or one row per sequence ([batch, n]; per-sequence layouts).
     `validate` sets ATTN_FLAG_VALIDATE (host check of cu_seqlens, segments and
     global positions). `heads_per_wg`, `order` ("natural", "xcd_groups") and
     `chunk` override the library's workgroup schedule (tuning and tests).
@@ -117,17 +135,17 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
     d.prefix_len, d.num_global, d.query_start = int(prefix_len), int(num_global), int(query_start)
     d.relative_position = 1 if relative_position else 0
     d.norm_kind = _NORMS[norm] if isinstance(norm, str) else int(norm)
+    nseq = (cu_seqlens_q.numel() - 1) if varlen else q.shape[0]
     if segment_starts is not None:
-        _int_array(segment_starts, "segment_starts", q.device)
+        d.num_segments, d.segment_stride = _layout_array(segment_starts, "segment_starts",
+                                                         q.device, nseq)
         d.segment_starts = segment_starts.data_ptr()
-        d.num_segments = segment_starts.numel()
     if global_tokens is not None:
-        _int_array(global_tokens, "global_tokens", q.device)
-        if num_global and int(num_global) != global_tokens.numel():
-            raise ValueError(f"num_global={num_global} but global_tokens has "
-                             f"{global_tokens.numel()} entries")
-        d.num_global = global_tokens.numel()
-        d.global_tokens = global_tokens.data_ptr() if global_tokens.numel() else None
+        n, d.global_stride = _layout_array(global_tokens, "global_tokens", q.device, nseq)
+        if num_global and int(num_global) != n:
+            raise ValueError(f"num_global={num_global} but global_tokens has {n} entries")
+        d.num_global = n
+        d.global_tokens = global_tokens.data_ptr() if n else None
     d.softcap = float(softcap)
     if alibi_slopes is not None:
         d.alibi_slopes = alibi_slopes.data_ptr()

@@ -12,7 +12,7 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libattn.so")
 
-ATTN_ABI_VERSION = 3
+ATTN_ABI_VERSION = 4
 ATTN_MAX_SEGMENTS = 2048
 ATTN_FLAG_VALIDATE = 1
 ATTN_BF16, ATTN_FP32 = 0, 1
@@ -76,6 +76,8 @@ class AttnVariantDesc(ctypes.Structure):
         ("sched_heads_per_wg", ctypes.c_int32),
         ("sched_order", ctypes.c_int32),
         ("sched_chunk", ctypes.c_int32),
+        ("segment_stride", ctypes.c_int64),
+        ("global_stride", ctypes.c_int64),
     ]
 
     @classmethod

@@ -119,15 +119,19 @@ int validate_device_inputs(const attn_variant_desc& d, bool varlen, bool segment
             }
         }
     }
-    if (segments) {
-        if (!fetch_i32(d.segment_starts, d.num_segments, stream, &a)) return ATTN_ERR_LAUNCH;
-        if (!strictly_increasing_nonneg(a)) return ATTN_ERR_BAD_VARIANT;
-    }
-    if (glist) {
-        if (!fetch_i32(d.global_tokens, d.num_global, stream, &a)) return ATTN_ERR_LAUNCH;
-        if (!strictly_increasing_nonneg(a)) return ATTN_ERR_BAD_VARIANT;
-    }
-    return ATTN_OK;
+    // one array, or one per sequence (a stride apart)
+    auto check_arrays = [&](const int32_t* base, int64_t n, int64_t stride) {
+        const int64_t copies = stride > 0 ? d.batch : 1;
+        for (int64_t s = 0; s < copies; ++s) {
+            if (!fetch_i32(base + s * stride, n, stream, &a)) return ATTN_ERR_LAUNCH;
+            if (!strictly_increasing_nonneg(a)) return ATTN_ERR_BAD_VARIANT;
+        }
+        return ATTN_OK;
+    };
+    int rc = ATTN_OK;
+    if (segments) rc = check_arrays(d.segment_starts, d.num_segments, d.segment_stride);
+    if (rc == ATTN_OK && glist) rc = check_arrays(d.global_tokens, d.num_global, d.global_stride);
+    return rc;
 }
 
 }  // namespace
@@ -209,6 +213,14 @@ static int check_variant(const attn_variant_desc* d)
         d->num_global > ATTN_MAX_SEGMENTS)
         return ATTN_ERR_BAD_VARIANT;
     if (d->flags & ~ATTN_FLAG_VALIDATE) return ATTN_ERR_BAD_VARIANT;
+    // per-sequence layouts: whole arrays a stride apart
+    if (d->segment_stride < 0 || d->global_stride < 0) return ATTN_ERR_BAD_VARIANT;
+    if (segment_mask(d->mask_kind) && d->segment_stride > 0 &&
+        d->segment_stride < d->num_segments)
+        return ATTN_ERR_BAD_VARIANT;
+    if (d->mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d->global_tokens &&
+        d->global_stride > 0 && d->global_stride < d->num_global)
+        return ATTN_ERR_BAD_VARIANT;
     return ATTN_OK;
 }
 
@@ -362,6 +374,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.num_global = d.num_global;
     p.seg = segment_mask(d.mask_kind) ? d.segment_starts : nullptr;
     p.num_seg = segment_mask(d.mask_kind) ? d.num_segments : 0;
+    p.seg_stride = segment_mask(d.mask_kind) ? d.segment_stride : 0;
     p.query_start = d.query_start;
     p.norm = d.norm_kind;
     p.relpos = d.relative_position;
@@ -480,6 +493,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     const bool glist = d.mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d.global_tokens &&
                        d.num_global > 0;
     p.gtok = glist ? d.global_tokens : nullptr;
+    p.gtok_stride = glist ? d.global_stride : 0;
     p.glob_items = 0;
     p.glob_chunks = 1;
     if (glist && d.dtype == ATTN_BF16) {

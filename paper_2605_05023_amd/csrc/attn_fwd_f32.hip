@@ -103,13 +103,16 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     __syncthreads();
 
     const int qi = q0 + lane;  // every wave covers the same 64 rows
+    // this sequence's index-mask layout (one shared by all when the stride is 0)
+    const int32_t* gtok = p.gtok ? p.gtok + (int64_t)b * p.gtok_stride : nullptr;
+    const int32_t* seg = p.seg ? p.seg + (int64_t)b * p.seg_stride : nullptr;
     RowVis rv = {0, 1, 0};
     int t_lo, t_hi;  // key tiles visited
     if constexpr (GEN) {
         if (qi < lq)
-            rv = p.gtok ? row_vis_listed(p.band, p.gtok, p.num_global, qi, lq, lk)
-                        : row_visibility(p.mask_kind, p.band, p.num_global, p.seg, p.num_seg,
-                                         p.query_start, qi, lq, lk);
+            rv = gtok ? row_vis_listed(p.band, gtok, p.num_global, qi, lq, lk)
+                      : row_visibility(p.mask_kind, p.band, p.num_global, seg, p.num_seg,
+                                       p.query_start, qi, lq, lk);
         const bool any = rv.pfx > 0 || rv.jlo <= rv.jhi;
         const int first = any ? (rv.pfx > 0 ? 0 : rv.jlo) : 0x3fffffff;
         const int last = any ? (rv.jlo <= rv.jhi ? rv.jhi : rv.pfx - 1) : -1;
@@ -125,9 +128,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     const int ip = qi + (lk - lq);
     // relative-position reference (see score_u): first visible key for softmax
     int jref = SOFTMAX ? (rv.pfx > 0 ? 0 : rv.jlo) : ip;
-    if (GEN && SOFTMAX && p.gtok) {  // the smallest visible key may be one of G
+    if (GEN && SOFTMAX && gtok) {  // the smallest visible key may be one of G
         int jr = rv.jlo <= rv.jhi ? rv.jlo : 0x7fffffff;
-        if (p.num_global > 0 && p.gtok[0] < lk) jr = min(jr, p.gtok[0]);
+        if (p.num_global > 0 && gtok[0] < lk) jr = min(jr, gtok[0]);
         jref = jr == 0x7fffffff ? 0 : jr;
     }
     float bias_abs = 0.0f, bias_lin = 0.0f;
@@ -173,10 +176,16 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
             s[j] = x;
             mx = __builtin_fmaxf(mx, x);
         }
-        float alpha = 1.0f, m_new = m_run;
+        float alpha = 1.0f, m_new = m_run, m_use = 0.0f;
         if constexpr (SOFTMAX) {
+            // A row that has seen no key yet (m_run = -inf) and sees none of
+            // this tile either (a gathered tile of global keys all inside its
+            // band or past the end) keeps m = -inf with O and l at 0: the
+            // exponentials take 0 in place of the max, where
+            // exp2(-inf - (-inf)) would be NaN.
             m_new = __builtin_fmaxf(m_run, mx);
-            alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 when m_run = -inf
+            m_use = m_new == -__builtin_inff() ? 0.0f : m_new;
+            alpha = __builtin_amdgcn_exp2f(m_run - m_use);  // 0 when only m_run = -inf
             m_run = m_new;
             l_run *= alpha;
 #pragma unroll
@@ -186,7 +195,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
         for (int j = 0; j < BN; ++j) {
             float pe;
             if constexpr (SOFTMAX) {
-                pe = __builtin_amdgcn_exp2f(s[j] - m_new);
+                pe = __builtin_amdgcn_exp2f(s[j] - m_use);
                 l_run += pe;
             } else {
                 pe = activation<NORM>(s[j]);  // the 1/L comes at the end
@@ -230,10 +239,10 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
     }
     // A listed global set (global sliding window): its keys outside the row's
     // band, BN list entries per tile, the waves taking turns.
-    if (GEN && p.gtok) {
+    if (GEN && gtok) {
         const int ng = p.num_global;
         for (int g0 = wave * BN; g0 < ng; g0 += NW * BN) {
-            auto key = [&](int r) { return g0 + r < ng ? min(p.gtok[g0 + r], lk) : lk; };
+            auto key = [&](int r) { return g0 + r < ng ? min(gtok[g0 + r], lk) : lk; };
             stage(key);
             consume(key, [&](int j) {
                 const int kj = key(j);

@@ -1126,10 +1126,12 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     // list entry wg_rows * chunk + 32*rblk + li), dims 16t + 8lh .. +7.
     int qi = q0 + rblk * 32 + li;
     bool row_ok = qi < lq;  // the row exists and this workgroup writes it
+    // this sequence's index-mask layout (one shared by all when the stride is 0)
+    [[maybe_unused]] const int32_t* gtok = p.gtok ? p.gtok + (int64_t)it.b * p.gtok_stride : nullptr;
     if constexpr (T::GLIST) {
         if (gmode) {
             const int k = it.qt * p.wg_rows + rblk * 32 + li;
-            qi = k < p.num_global ? p.gtok[k] - (lk - lq) : -1;
+            qi = k < p.num_global ? gtok[k] - (lk - lq) : -1;
             row_ok = qi >= 0 && qi < lq;
             if (!row_ok) qi = 0;  // (its Q load stays in range; nothing is written)
         }
@@ -1185,17 +1187,17 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     int ng = 0;
     if constexpr (T::GEN) {
         __shared__ int red[4][8];
-        const int32_t* seg = p.seg;
-        if (p.seg) {  // stage the segment starts in the (not yet used) V buffer 1
+        const int32_t* seg = p.seg ? p.seg + (int64_t)it.b * p.seg_stride : nullptr;
+        if (seg) {  // stage the segment starts in the (not yet used) V buffer 1
             int32_t* sl = reinterpret_cast<int32_t*>(lds_v1);
-            for (int i = tid; i < p.num_seg; i += NT) sl[i] = p.seg[i];
+            for (int i = tid; i < p.num_seg; i += NT) sl[i] = seg[i];
             __syncthreads();
             seg = sl;
         }
         if constexpr (T::GLIST) {
             ng = p.num_global;
             const int npad = (ng + BN - 1) / BN * BN;
-            for (int i = tid; i < npad; i += NT) gl[i] = i < ng ? p.gtok[i] : lk;
+            for (int i = tid; i < npad; i += NT) gl[i] = i < ng ? gtok[i] : lk;
             __syncthreads();
         }
         RowVis rv = {0, 1, 0};

@@ -65,6 +65,9 @@ struct AttnParams {
                              // positions 0..num_global-1
     const int32_t* seg;      // segment start positions (device), or null
     int32_t num_seg;
+    // elements between the segment starts (global positions) of consecutive
+    // sequences; 0 = one layout for all
+    int64_t seg_stride, gtok_stride;
     int32_t query_start;     // causal blockwise: first test-query position
     int32_t norm;            // attn_norm_kind_t
     int32_t relpos;          // add (i' - j) to the score

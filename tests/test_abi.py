@@ -147,6 +147,18 @@ CASES = [
                                              setattr(d, "num_global", _abi.ATTN_MAX_SEGMENTS + 1)),
      "ATTN_ERR_BAD_VARIANT"),
     ("unknown flag", lambda d: setattr(d, "flags", 2), "ATTN_ERR_BAD_VARIANT"),
+    ("negative segment stride", lambda d: (setattr(d, "mask_kind", 5), setattr(d, "segment_starts", P),
+                                           setattr(d, "num_segments", 3),
+                                           setattr(d, "segment_stride", -3)), "ATTN_ERR_BAD_VARIANT"),
+    ("segment rows overlap", lambda d: (setattr(d, "mask_kind", 6), setattr(d, "segment_starts", P),
+                                        setattr(d, "num_segments", 3),
+                                        setattr(d, "segment_stride", 2)), "ATTN_ERR_BAD_VARIANT"),
+    ("negative global stride", lambda d: (setattr(d, "mask_kind", 4), setattr(d, "global_tokens", P),
+                                          setattr(d, "num_global", 3),
+                                          setattr(d, "global_stride", -1)), "ATTN_ERR_BAD_VARIANT"),
+    ("global rows overlap", lambda d: (setattr(d, "mask_kind", 4), setattr(d, "global_tokens", P),
+                                       setattr(d, "num_global", 3),
+                                       setattr(d, "global_stride", 1)), "ATTN_ERR_BAD_VARIANT"),
     ("heads per wg 3", lambda d: setattr(d, "sched_heads_per_wg", 3), "ATTN_ERR_BAD_VARIANT"),
     ("heads per wg 8", lambda d: setattr(d, "sched_heads_per_wg", 8), "ATTN_ERR_BAD_VARIANT"),
     ("heads per wg not dividing", lambda d: (setattr(d, "num_q_heads", 6), setattr(d, "num_kv_heads", 3),
@@ -262,3 +274,23 @@ def test_row_range_rejects_listed_global_set(lib):
     d.global_tokens = None  # leading run: prefix plus band
     assert lib.attn_row_range(ctypes.byref(d), None, 5, 10, 10, out) == 0
     assert tuple(out) == (0, 0, 9)  # prefix {0,1,2} touches the band [1, 9]: merged
+
+
+def test_per_sequence_layout_strides_accepted(lib):
+    """A stride of at least the entry count (one row per sequence) passes the
+    host checks and the call reaches the pointer check."""
+    d = base_desc()
+    d.mask_kind = _abi.ATTN_MASK_SHARE_QUESTION
+    d.segment_starts = P
+    d.num_segments = 3
+    d.segment_stride = 3
+    assert call(lib, d, q=None) == err("ATTN_ERR_NULL_PTR")
+    d.segment_stride = 16  # padded rows
+    assert call(lib, d, q=None) == err("ATTN_ERR_NULL_PTR")
+    d = base_desc()
+    d.mask_kind = _abi.ATTN_MASK_GLOBAL_SLIDING_WINDOW
+    d.window_left = d.window_right = 4
+    d.global_tokens = P
+    d.num_global = 5
+    d.global_stride = 5
+    assert call(lib, d, q=None) == err("ATTN_ERR_NULL_PTR")

@@ -134,3 +134,41 @@ def test_fwd_refuses_host_tensors():
     t = fixed()
     with pytest.raises(ValueError):
         attn.fwd(t["q"], t["k"], t["v"], causal=True)
+
+
+def test_per_sequence_layouts():
+    """segment_starts / global_tokens: one array shared by every sequence, or
+    one row per sequence ([batch, n]) whose row stride becomes the
+    descriptor's stride."""
+    seg = torch.tensor([10, 20, 30], dtype=torch.int32)
+    d = desc(fixed(), mask="share_question", segment_starts=seg)
+    assert (d.num_segments, d.segment_stride) == (3, 0)
+    rows = torch.tensor([[10, 20, 30], [5, 6, 99]], dtype=torch.int32)
+    d = desc(fixed(), mask="causal_blockwise", segment_starts=rows)
+    assert (d.num_segments, d.segment_stride) == (3, 3)
+    padded = torch.zeros((2, 8), dtype=torch.int32)[:, :3]  # rows 8 apart
+    d = desc(fixed(), mask="share_question", segment_starts=padded)
+    assert (d.num_segments, d.segment_stride) == (3, 8)
+    g = torch.tensor([[0, 50], [3, 7]], dtype=torch.int32)
+    d = varlen_desc(packed(), mask="global_sliding_window", window=(4, 4), global_tokens=g)
+    assert (d.num_global, d.global_stride) == (2, 2)
+
+
+PERSEQ_BAD = [
+    ("rows != batch", dict(mask="share_question",
+                           segment_starts=torch.zeros((3, 2), dtype=torch.int32)), ValueError),
+    ("rank 3", dict(mask="share_question",
+                    segment_starts=torch.zeros((2, 2, 2), dtype=torch.int32)), ValueError),
+    ("column-major rows", dict(mask="share_question",
+                               segment_starts=torch.zeros((4, 2), dtype=torch.int32).t()),
+     ValueError),
+    ("global rows != batch", dict(mask="global_sliding_window", window=(4, 4),
+                                  global_tokens=torch.zeros((1, 2), dtype=torch.int32)), ValueError),
+    ("int64 rows", dict(mask="share_question", segment_starts=torch.zeros((2, 2))), TypeError),
+]
+
+
+@pytest.mark.parametrize("name,kw,exc", PERSEQ_BAD, ids=[c[0] for c in PERSEQ_BAD])
+def test_per_sequence_layout_errors(name, kw, exc):
+    with pytest.raises(exc):
+        desc(fixed(), **kw)
