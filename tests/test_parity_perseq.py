@@ -16,7 +16,7 @@ import oracle
 from gpu_util import LSE_TOL, O_TOL, gpu_available, log
 from paper_2605_05023_amd import fwd
 from paper_2605_05023_amd.workloads import (MASK_CAUSAL_BLOCKWISE, MASK_GLOBAL_WINDOW, MASK_NAMES,
-                                            MASK_SHARE_QUESTION)
+                                            MASK_SHARE_QUESTION, alibi_slopes)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
@@ -68,10 +68,14 @@ def _run(c, rows_layout, shared=None):
         qs, ks = (sum(lens), hq, D), (sum(lens), hkv, D)
     else:
         qs, ks = (B, hq, lens[0], D), (B, hkv, lens[0], D)
-    q = torch.randn(qs, generator=g).to(tdt)
-    k = torch.randn(ks, generator=g).to(tdt)
+    sigma = 1.5 if (extra.get("alibi") or extra.get("softcap")) else 1.0
+    q = (torch.randn(qs, generator=g) * sigma).to(tdt)
+    k = (torch.randn(ks, generator=g) * sigma).to(tdt)
     v = torch.randn(ks, generator=g).to(tdt)
-    kw = dict(mask=MASK_NAMES[mask], norm=norm, query_start=extra.get("query_start", 0))
+    kw = dict(mask=MASK_NAMES[mask], norm=norm, query_start=extra.get("query_start", 0),
+              softcap=extra.get("softcap", 0.0), relative_position=extra.get("relpos", False))
+    if extra.get("alibi"):
+        kw["alibi_slopes"] = alibi_slopes(hq).to(DEV)
     if "window" in extra:
         kw["window"] = extra["window"]
     cu = None
@@ -88,6 +92,51 @@ def _run(c, rows_layout, shared=None):
     torch.cuda.synchronize()
     o, lse = res if isinstance(res, tuple) else (res, None)
     return q, k, v, cu, o, lse
+
+
+def _draw_random(n=24, seed=5023):
+    """Seeded random per-sequence cases: index mask, fixed or packed lengths,
+    per-sequence rows (some entries at or past the sequence end), head dim,
+    group size, dtype, normalisation, ALiBi, relative position, soft-cap."""
+    rng = np.random.default_rng(seed)
+    masks = [MASK_SHARE_QUESTION, MASK_CAUSAL_BLOCKWISE, MASK_GLOBAL_WINDOW]
+    out = []
+    for i in range(n):
+        mask = masks[i % 3]
+        varlen = bool(rng.random() < 0.5)
+        nseq = int(rng.integers(2, 5))
+        lens = [int(rng.integers(1, 350)) for _ in range(nseq)] if varlen else \
+            [int(rng.integers(1, 350))] * nseq
+        cnt = int(rng.integers(1, 6))
+        rows = []
+        for L in lens:  # strictly increasing, within [0, L + 40)
+            rows.append(sorted(rng.choice(L + 40, size=cnt, replace=False).tolist()))
+        extra = {}
+        if mask == MASK_GLOBAL_WINDOW:
+            extra["window"] = (int(rng.integers(0, 60)), int(rng.choice([0, int(rng.integers(0, 60))])))
+        if mask == MASK_CAUSAL_BLOCKWISE:
+            extra["query_start"] = int(rng.integers(0, max(lens) + 1))
+        extra["alibi"] = bool(rng.random() < 0.25)
+        extra["relpos"] = bool(rng.random() < 0.2)
+        extra["softcap"] = float(rng.choice([0.0, 0.0, 0.0, 30.0, 400.0]))
+        dtype = "fp32" if rng.random() < 0.2 else "bf16"
+        norm = str(rng.choice(["softmax"] * 4 + ["relu", "sigmoid"]))
+        D = int(rng.choice([64, 128]))
+        group = int(rng.choice([1, 2, 4]))
+        hkv = int(rng.integers(1, 3))
+        name = (f"rnd{seed}_{i:02d}_{MASK_NAMES[mask]}_{'varlen' if varlen else 'fixed'}_{dtype}"
+                f"_d{D}_g{group}_{norm}")
+        out.append((name, mask, lens, varlen, D, group * hkv, hkv, dtype, norm, rows, extra))
+    return out
+
+
+RANDOM = _draw_random()
+
+
+@pytest.mark.parametrize("c", RANDOM, ids=[c[0] for c in RANDOM])
+def test_per_sequence_layout_random(c):
+    log(f"[parity per-sequence layout, random] {c[0]} lengths={c[2]} rows={c[9]} extra={c[10]}")
+    _check(c, c[9], *_run(c, c[9]))
 
 
 @pytest.mark.parametrize("c", CASES, ids=[c[0] for c in CASES])
@@ -136,7 +185,9 @@ def _check(c, rows, q, k, v, cu, o, lse):
             l_s = lg[s] if lg is not None else None
         n = ks_.shape[2]
         okw = dict(query_start=extra.get("query_start", 0),
-                   norm={"softmax": 0, "relu": 1, "sigmoid": 2}[norm])
+                   norm={"softmax": 0, "relu": 1, "sigmoid": 2}[norm],
+                   softcap=extra.get("softcap", 0.0), relpos=extra.get("relpos", False),
+                   slopes=alibi_slopes(hq) if extra.get("alibi") else None)
         wl_, wr_ = extra.get("window", (-1, -1))
         if mask == MASK_GLOBAL_WINDOW:
             okw["global_tokens"] = list(layout)
