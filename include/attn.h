@@ -58,8 +58,13 @@ extern "C" {
  *   a violation returns ATTN_ERR_BAD_SHAPE (cu_seqlens) or
  *   ATTN_ERR_BAD_VARIANT (segments, global positions) and nothing is
  *   enqueued. A debugging aid: it costs a host round trip per call.
+ * ATTN_FLAG_LOG: print one line per enqueued call to stderr naming the
+ *   kernel variant and its launch plan (grid, rows and heads per workgroup,
+ *   workgroup order, soft-cap form), and one line for a failed launch.
+ *   Nothing is printed without it.
  */
 #define ATTN_FLAG_VALIDATE 1u
+#define ATTN_FLAG_LOG 2u
 
 typedef enum attn_dtype {
     ATTN_BF16 = 0, /* q, k, v, out are bfloat16; accumulation in fp32 */

@@ -17,7 +17,7 @@ from typing import Optional
 
 import torch
 
-from ._abi import (ATTN_BF16, ATTN_FLAG_VALIDATE, ATTN_FP32, ATTN_MASK_CAUSAL,  # noqa: F401
+from ._abi import (ATTN_BF16, ATTN_FLAG_LOG, ATTN_FLAG_VALIDATE, ATTN_FP32, ATTN_MASK_CAUSAL,  # noqa: F401
                    ATTN_MASK_CAUSAL_BLOCKWISE, ATTN_MASK_GLOBAL_SLIDING_WINDOW, ATTN_MASK_NONE,
                    ATTN_MASK_PREFIX_LM, ATTN_MASK_SHARE_QUESTION, ATTN_MASK_SLIDING_WINDOW,
                    ATTN_MAX_SEGMENTS, ATTN_NORM_RELU, ATTN_NORM_SIGMOID, ATTN_NORM_SOFTMAX,
@@ -27,7 +27,7 @@ __all__ = ["fwd", "make_desc", "lse_shape", "AttnError", "AttnVariantDesc", "loa
            "row_range", "ATTN_BF16", "ATTN_FP32", "ATTN_MASK_NONE", "ATTN_MASK_CAUSAL",
            "ATTN_MASK_SLIDING_WINDOW", "ATTN_MASK_PREFIX_LM", "ATTN_MASK_GLOBAL_SLIDING_WINDOW",
            "ATTN_MASK_SHARE_QUESTION", "ATTN_MASK_CAUSAL_BLOCKWISE", "ATTN_NORM_SOFTMAX",
-           "ATTN_NORM_RELU", "ATTN_NORM_SIGMOID", "ATTN_FLAG_VALIDATE"]
+           "ATTN_NORM_RELU", "ATTN_NORM_SIGMOID", "ATTN_FLAG_VALIDATE", "ATTN_FLAG_LOG"]
 
 _DTYPES = {torch.bfloat16: ATTN_BF16, torch.float32: ATTN_FP32}
 _MASKS = {"none": ATTN_MASK_NONE, "causal": ATTN_MASK_CAUSAL,
@@ -99,7 +99,7 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
               max_seqlen_k=None, stream=None, mask=None, prefix_len=0, num_global=0,
               global_tokens=None, segment_starts=None, query_start=0, relative_position=False,
               norm="softmax", validate=False, heads_per_wg=0, order=None,
-              chunk=0) -> AttnVariantDesc:
+              chunk=0, log=False) -> AttnVariantDesc:
     """Build the descriptor for tensors q/k/v/out (see include/attn.h for layouts).
 
     `mask` names any attn_mask_kind_t ("prefix_lm", "global_sliding_window",
@@ -110,7 +110,7 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
     `segment_starts` and `global_tokens` are one array shared by every
     sequence, or one row per sequence ([batch, n]; per-sequence layouts).
     `validate` sets ATTN_FLAG_VALIDATE (host check of cu_seqlens, segments and
-    global positions). `heads_per_wg`, `order` ("natural", "xcd_groups") and
+    global positions), `log` ATTN_FLAG_LOG (the launch plan on stderr). `heads_per_wg`, `order` ("natural", "xcd_groups") and
     `chunk` override the library's workgroup schedule (tuning and tests).
     """
     if q.dtype not in _DTYPES or k.dtype != q.dtype or v.dtype != q.dtype or out.dtype != q.dtype:
@@ -174,7 +174,7 @@ def make_desc(q, k, v, out, *, causal=False, window=None, alibi_slopes=None, sof
             setattr(d, f"stride_{name}_b", t.stride(0))
             setattr(d, f"stride_{name}_h", t.stride(1))
             setattr(d, f"stride_{name}_s", t.stride(2))
-    d.flags = ATTN_FLAG_VALIDATE if validate else 0
+    d.flags = (ATTN_FLAG_VALIDATE if validate else 0) | (ATTN_FLAG_LOG if log else 0)
     d.sched_heads_per_wg = int(heads_per_wg)
     d.sched_order = _ORDERS[order]
     d.sched_chunk = int(chunk)
@@ -189,7 +189,8 @@ def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softca
         max_seqlen_k=None, out=None, lse=None, return_lse: bool = True, mask=None,
         prefix_len: int = 0, num_global: int = 0, global_tokens=None, segment_starts=None,
         query_start: int = 0, relative_position: bool = False, norm="softmax",
-        validate: bool = False, heads_per_wg: int = 0, order=None, chunk: int = 0):
+        validate: bool = False, heads_per_wg: int = 0, order=None, chunk: int = 0,
+        log: bool = False):
     """Attention forward on the GPU.
 
     Fixed length: q [B,Hq,S,D], k/v [B,Hkv,Sk,D] -> out like q, lse [B,Hq,S] fp32.
@@ -223,7 +224,7 @@ def fwd(q, k, v, *, causal: bool = False, window=None, alibi_slopes=None, softca
                   num_global=num_global, global_tokens=global_tokens,
                   segment_starts=segment_starts, query_start=query_start,
                   relative_position=relative_position, norm=norm, validate=validate,
-                  heads_per_wg=heads_per_wg, order=order, chunk=chunk)
+                  heads_per_wg=heads_per_wg, order=order, chunk=chunk, log=log)
     status = lib.attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                           lse.data_ptr() if lse is not None else None, ctypes.byref(d))
     check(status, lib)

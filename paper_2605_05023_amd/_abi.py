@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_HERE, "libattn.so")
 ATTN_ABI_VERSION = 4
 ATTN_MAX_SEGMENTS = 2048
 ATTN_FLAG_VALIDATE = 1
+ATTN_FLAG_LOG = 2
 ATTN_BF16, ATTN_FP32 = 0, 1
 ATTN_MASK_NONE, ATTN_MASK_CAUSAL, ATTN_MASK_SLIDING_WINDOW = 0, 1, 2
 ATTN_MASK_PREFIX_LM, ATTN_MASK_GLOBAL_SLIDING_WINDOW = 3, 4

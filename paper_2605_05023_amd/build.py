@@ -1,9 +1,12 @@
 """Build libattn.so (HIP kernels for gfx950 plus the C ABI) in-tree.
 
-    python -m paper_2605_05023_amd.build
+    python -m paper_2605_05023_amd.build               # libattn.so
+    python -m paper_2605_05023_amd.build --lds-poison  # libattn_poison.so
 
 Each translation unit is compiled to an object in parallel, then linked.
-Packed fp32 instructions are disabled for all device code.
+Packed fp32 instructions are disabled for all device code. The LDS-poisoning
+debug build (ATTN_LDS_POISON, kernel_params.h) fills every kernel's LDS with
+all-ones bytes first; tests compare it with the release build bit for bit.
 """
 from __future__ import annotations
 
@@ -17,6 +20,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libattn.so")
+LIB_POISON = os.path.join(PKG, "libattn_poison.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 ARCH = "gfx950"
 
@@ -37,9 +41,11 @@ def sources():
                   if f.endswith((".hip", ".cpp")))
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc(), *COMMON, *DEVICE_FLAGS, "-c", src, "-o", obj]
+def _compile(src: str, poison: bool = False) -> str:
+    bdir = BUILD_DIR + ("_poison" if poison else "")
+    obj = os.path.join(bdir, os.path.basename(src) + ".o")
+    extra = ["-DATTN_LDS_POISON=1"] if poison else []
+    cmd = [hipcc(), *COMMON, *DEVICE_FLAGS, *extra, "-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     # hipcc's host pass does not know the device-only feature flag; drop that note
     err = "\n".join(l for l in res.stderr.splitlines()
@@ -51,19 +57,20 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
+def build(verbose: bool = False, poison: bool = False) -> str:
+    lib = LIB_POISON if poison else LIB
+    os.makedirs(BUILD_DIR + ("_poison" if poison else ""), exist_ok=True)
     srcs = sources()
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, poison), srcs))
+    tmp = lib + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {lib}")
+    return lib
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    build(verbose=True, poison="--lds-poison" in sys.argv[1:])

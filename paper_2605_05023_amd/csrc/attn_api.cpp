@@ -8,6 +8,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
 #include <vector>
 
 #include "../../include/attn.h"
@@ -134,6 +135,35 @@ int validate_device_inputs(const attn_variant_desc& d, bool varlen, bool segment
     return rc;
 }
 
+// ATTN_FLAG_LOG: the kernel variant and launch plan of one call, on stderr
+// (the variant follows the dispatch of launch_bf16 / launch_f32).
+void log_plan(const attn_variant_desc& d, const AttnParams& p)
+{
+    static const char* masks[] = {"none", "causal", "sliding_window", "prefix_lm",
+                                  "global_sliding_window", "share_question", "causal_blockwise"};
+    static const char* norms[] = {"softmax", "relu", "sigmoid"};
+    const bool closed = d.mask_kind >= ATTN_MASK_NONE && d.mask_kind <= ATTN_MASK_PREFIX_LM;
+    const bool both = p.slopes && p.relpos;
+    const char* path = p.gtok ? "general, listed global set"
+                       : (d.norm_kind != ATTN_NORM_SOFTMAX || !closed || both) ? "general"
+                       : p.band.wl >= 0 ? "closed-form band with a left bound"
+                                        : "closed-form band, running max checked through the row sums";
+    const char* cap = d.softcap <= 0.0f                          ? "off"
+                      : d.softcap <= 256.0f && p.cap_zmax >= 0.0f ? "short form, polynomial where in range"
+                      : d.softcap <= 256.0f                       ? "short form"
+                                                                  : "exact";
+    const char* order = p.map_mode == 1 ? "kv groups per XCD" : "natural";
+    std::fprintf(stderr,
+                 "attn_fwd: %s D=%d B=%d Hq=%d Hkv=%d %s mask=%s norm=%s alibi=%d relpos=%d "
+                 "softcap=%g (%s) | %s kernel, grid %d, %d rows x %d heads per workgroup, "
+                 "order %s, chunk %d%s, global-row items %d\n",
+                 d.dtype == ATTN_BF16 ? "bf16" : "fp32", d.head_dim, d.batch, d.num_q_heads,
+                 d.num_kv_heads, p.cu_q ? "varlen" : "fixed-length", masks[d.mask_kind],
+                 norms[d.norm_kind], p.slopes != nullptr, p.relpos, (double)d.softcap, cap,
+                 d.dtype == ATTN_BF16 ? path : "fp32", p.grid, p.wg_rows, p.hp, order, p.chunk,
+                 p.compact ? ", packed grid" : "", p.glob_items);
+}
+
 }  // namespace
 
 static_assert(ATTN_MAX_SEGMENTS == kMaxGlobalList, "LDS staging of the listed global set");
@@ -212,7 +242,7 @@ static int check_variant(const attn_variant_desc* d)
     if (d->mask_kind == ATTN_MASK_GLOBAL_SLIDING_WINDOW && d->global_tokens &&
         d->num_global > ATTN_MAX_SEGMENTS)
         return ATTN_ERR_BAD_VARIANT;
-    if (d->flags & ~ATTN_FLAG_VALIDATE) return ATTN_ERR_BAD_VARIANT;
+    if (d->flags & ~(ATTN_FLAG_VALIDATE | ATTN_FLAG_LOG)) return ATTN_ERR_BAD_VARIANT;
     // per-sequence layouts: whole arrays a stride apart
     if (d->segment_stride < 0 || d->global_stride < 0) return ATTN_ERR_BAD_VARIANT;
     if (segment_mask(d->mask_kind) && d->segment_stride > 0 &&
@@ -508,7 +538,10 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
         if (rc != ATTN_OK) return rc;
     }
     hipStream_t stream = static_cast<hipStream_t>(d.stream);
+    if (d.flags & ATTN_FLAG_LOG) log_plan(d, p);
     hipError_t err = d.dtype == ATTN_BF16 ? attn::launch_bf16(p, d.head_dim, stream)
                                           : attn::launch_f32(p, d.head_dim, stream);
+    if (err != hipSuccess && (d.flags & ATTN_FLAG_LOG))
+        std::fprintf(stderr, "attn_fwd: launch failed: %s\n", hipGetErrorString(err));
     return err == hipSuccess ? ATTN_OK : ATTN_ERR_LAUNCH;
 }

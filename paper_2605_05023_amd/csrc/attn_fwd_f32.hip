@@ -57,6 +57,12 @@ __global__ __launch_bounds__(NT) void attn_fwd_f32_kernel(AttnParams p)
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    if constexpr (kLdsPoison) {
+        for (int i = tid; i < (int)(sizeof(qs) / 4); i += NT) (&qs[0][0])[i] = __builtin_bit_cast(float, ~0u);
+        for (int i = tid; i < (int)(sizeof(lds) / 4); i += NT)
+            reinterpret_cast<uint32_t*>(lds)[i] = ~0u;
+        __syncthreads();
+    }
     const int nbh = p.batch * p.hq;
     const int w = blockIdx.x;
     const int qt = p.q_order ? w / nbh : p.num_q_tiles - 1 - w / nbh;

@@ -1042,8 +1042,21 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     __shared__ __attribute__((aligned(1024))) char lds_k1[T::TILE];
     __shared__ __attribute__((aligned(1024))) char lds_v0[T::TILE];
     __shared__ __attribute__((aligned(1024))) char lds_v1[T::TILE];
+    // listed global set: G in LDS, padded with lk to a multiple of BN
+    __shared__ __attribute__((aligned(16))) int gl[T::GLIST ? kMaxGlobalList + BN : 4];
 
     const int tid = threadIdx.x;
+    if constexpr (kLdsPoison) {
+        const u32x4 ones = {~0u, ~0u, ~0u, ~0u};
+        for (int i = tid; i < T::TILE / 16; i += NT) {
+            reinterpret_cast<u32x4*>(lds_k0)[i] = ones;
+            reinterpret_cast<u32x4*>(lds_k1)[i] = ones;
+            reinterpret_cast<u32x4*>(lds_v0)[i] = ones;
+            reinterpret_cast<u32x4*>(lds_v1)[i] = ones;
+        }
+        for (int i = tid; i < (int)(sizeof(gl) / sizeof(int)); i += NT) gl[i] = -1;
+        __syncthreads();
+    }
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int li = lane & 31, lh = lane >> 5;
 
@@ -1182,8 +1195,6 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_bf16_kernel(AttnParams p)
     TileRanges tr = {};
     int jbeg, jend;
     TilePlan gp = {};
-    // listed global set: G in LDS, padded with lk to a multiple of BN
-    __shared__ __attribute__((aligned(16))) int gl[T::GLIST ? kMaxGlobalList + BN : 4];
     int ng = 0;
     if constexpr (T::GEN) {
         __shared__ int red[4][8];

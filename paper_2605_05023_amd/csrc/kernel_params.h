@@ -10,6 +10,15 @@
 // Largest listed global set of the global sliding window (staged in LDS).
 constexpr int kMaxGlobalList = 2048;
 
+// Debug build (build.py --lds-poison): every kernel first fills its LDS
+// buffers with all-ones bytes (NaN in bf16 and fp32, -1 as an int), so that a
+// read of LDS no load or store wrote shows in the output; a correct kernel
+// gives the same bits as the release build.
+#ifndef ATTN_LDS_POISON
+#define ATTN_LDS_POISON 0
+#endif
+constexpr bool kLdsPoison = ATTN_LDS_POISON != 0;
+
 struct AttnParams {
     const void* q;
     const void* k;

@@ -146,7 +146,7 @@ CASES = [
     ("too many global positions", lambda d: (setattr(d, "mask_kind", 4), setattr(d, "global_tokens", P),
                                              setattr(d, "num_global", _abi.ATTN_MAX_SEGMENTS + 1)),
      "ATTN_ERR_BAD_VARIANT"),
-    ("unknown flag", lambda d: setattr(d, "flags", 2), "ATTN_ERR_BAD_VARIANT"),
+    ("unknown flag", lambda d: setattr(d, "flags", 4), "ATTN_ERR_BAD_VARIANT"),
     ("negative segment stride", lambda d: (setattr(d, "mask_kind", 5), setattr(d, "segment_starts", P),
                                            setattr(d, "num_segments", 3),
                                            setattr(d, "segment_stride", -3)), "ATTN_ERR_BAD_VARIANT"),

@@ -172,3 +172,10 @@ PERSEQ_BAD = [
 def test_per_sequence_layout_errors(name, kw, exc):
     with pytest.raises(exc):
         desc(fixed(), **kw)
+
+
+def test_log_flag():
+    d = desc(fixed(), causal=True, log=True)
+    assert d.flags == attn.ATTN_FLAG_LOG
+    d = desc(fixed(), causal=True, log=True, validate=True)
+    assert d.flags == attn.ATTN_FLAG_LOG | attn.ATTN_FLAG_VALIDATE
