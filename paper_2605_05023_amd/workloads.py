@@ -11,7 +11,9 @@ distribution. The five headline workloads keep that shape family and add the
 variants of Appendix A built in first; the further variants (PrefixLM,
 relative position, ReLU / Sigmoid normalisation, their combination, global
 sliding window, share question, causal blockwise) each get one workload at
-the Llama2-7B tuple 32/32/128 with S = 8k and B = 2 (16k tokens).
+the Llama2-7B tuple 32/32/128 with S = 8k and B = 2 (16k tokens). The
+`grid405b_*` workloads repeat the paper's comparison grid: the 128/8/128
+tuple at S = 1k..8k, 16k tokens per batch, four variants.
 
 Input recipe (identical on every machine because it uses the CPU generator):
     g = torch.Generator().manual_seed(seed)
@@ -122,10 +124,31 @@ NEXT_WORKLOADS = {
 }
 WORKLOADS.update(NEXT_WORKLOADS)
 
+
+def _grid405b(variant, seqlen, seed):
+    kw = {"causal": dict(mask=MASK_CAUSAL),
+          "window": dict(mask=MASK_SLIDING_WINDOW, window_left=1023, window_right=0),
+          "softcap": dict(mask=MASK_CAUSAL, softcap=50.0),
+          "alibi": dict(mask=MASK_CAUSAL, alibi=True)}[variant]
+    name = f"grid405b_{variant}_s{seqlen // 1024}k"
+    return name, Workload(name, "bf16", 16384 // seqlen, 128, 8, seqlen, 128, seed=seed, **kw)
+
+
+# The shape grid of the paper's comparison with a hand-written library
+# (Section 4.1 and Appendix C: the Llama3.1-405B attention tuple 128/8/128,
+# S = 1k..8k at 16k tokens per batch) for its four variants there. The paper
+# states neither the window nor the cap nor a mask for the soft-cap and ALiBi
+# rows: window (1023, 0), C = 50 and a causal mask are this module's choices.
+GRID_WORKLOADS = dict(_grid405b(v, s, 20 + 4 * i + j)
+                      for i, v in enumerate(("causal", "window", "softcap", "alibi"))
+                      for j, s in enumerate((1024, 2048, 4096, 8192)))
+WORKLOADS.update(GRID_WORKLOADS)
+
 # Order used when a list of the five headline workloads is wanted.
 WORKLOAD_ORDER = ["plain_fp32", "causal_bf16", "gqa_swa_bf16",
                   "alibi_softcap_bf16", "varlen_gqa_bf16"]
 NEXT_ORDER = list(NEXT_WORKLOADS)
+GRID_ORDER = list(GRID_WORKLOADS)
 
 
 @dataclasses.dataclass

@@ -73,3 +73,18 @@ def test_traffic_summary(name):
     stored = _field(text, "kernel_hash")
     current = bench.kernel_hash()
     assert bench.read_traffic(name) == (hbm if stored == current else None)
+
+
+def test_grid_pair_counts():
+    """The paper-grid workloads (16k tokens, 128 query heads): causal rows see
+    i + 1 keys, window rows min(i + 1, 1024)."""
+    import types
+    from paper_2605_05023_amd.workloads import GRID_ORDER, MASK_SLIDING_WINDOW
+    for name in GRID_ORDER:
+        wl = WORKLOADS[name]
+        S = wl.seqlen
+        per_seq = sum(min(i + 1, 1024) for i in range(S)) if wl.mask == MASK_SLIDING_WINDOW \
+            else S * (S + 1) // 2
+        inp = types.SimpleNamespace(wl=wl, lengths=None, segment_starts=None)
+        assert wl.batch * S == 16384 and (wl.hq, wl.hkv, wl.head_dim) == (128, 8, 128)
+        assert bench.visible_pairs(inp) == per_seq * wl.batch * 128, name
