@@ -817,7 +817,6 @@ __device__ __forceinline__ void pipelined_step(const char* kread, const char* vr
     static_for<PV>([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = ic.value;
         constexpr int b = i / (2 * DBLK), u = (i / DBLK) % 2, d = i % DBLK;
-        typedef short s16x8 __attribute__((ext_vector_type(8)));
         s16x8 a8 = __builtin_shufflevector(vlo[i], vhi[i], 0, 1, 2, 3, 4, 5, 6, 7);
         ws.oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a8),
                                                              __builtin_bit_cast(bf16x8, pw[b][u]),

@@ -360,6 +360,25 @@ def test_varlen_packed_grid(case):
     assert_parity(inp, o, lse, label=name)
 
 
+def test_packed_grid_by_default_for_skewed_batch(capfd):
+    """Without schedule overrides, a packed batch whose padded grid would be
+    mostly workgroups past their sequence's end (255 sequences of 1-32 tokens
+    beside one of 4096; K/V far below the chunking threshold) takes the packed
+    grid, and matches the oracle."""
+    g = torch.Generator().manual_seed(11)
+    lengths = torch.randint(1, 33, (256,), generator=g).tolist()
+    lengths[100] = 4096
+    wl = Workload("skewed_default", "bf16", len(lengths), 8, 2, 0, 128, mask=CAUSAL, seed=28,
+                  varlen=True)
+    inp = make_inputs(wl, lengths=lengths)
+    log(f"[parity packed grid] skewed default: T={inp.total_tokens}")
+    o, lse = run_gpu(inp, log=True)
+    torch.cuda.synchronize()
+    plan = [x for x in capfd.readouterr().err.splitlines() if x.startswith("attn_fwd:")]
+    assert len(plan) == 1 and ", packed grid" in plan[0] and "chunk 1" in plan[0], plan
+    assert_parity(inp, o, lse, rows=sample_rows(inp, 512, seed=2), label="skewed default")
+
+
 @pytest.mark.parametrize("hp,order", [(1, "natural"), (2, "natural"), (4, "natural"),
                                       (1, "xcd_groups"), (2, "xcd_groups"), (4, "xcd_groups")])
 def test_schedule_overrides(hp, order):
