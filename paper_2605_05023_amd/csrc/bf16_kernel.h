@@ -294,23 +294,34 @@ struct Bool {
 // (ceil(length / 128) spans of hp tiles, times its head sets), in the same
 // order inside the group as the padded grid, so no workgroup is spent on
 // tiles past a sequence's end. Every wave finds its group from the prefix
-// sums of the item counts over the XCD's groups, 64 groups at a time.
+// sums of the item counts over the XCD's groups, 256 groups at a time (four
+// consecutive groups per lane, their length loads issued together, so a batch
+// of thousands of sequences waits on a quarter of the load round trips).
 __device__ __forceinline__ WorkItem decode_packed(const AttnParams& p, uint32_t uw)
 {
+    constexpr int PER = 4;  // groups per lane and round
     WorkItem it = {0, 0, 0, -1};
     const uint32_t x = uw & 7, k = uw >> 3;
     const int lane = __lane_id();
-    uint32_t base = 0;  // items of the groups before this block of 64
-    for (int i0 = 0; i0 < p.groups_per_xcd; i0 += 64) {
-        const int i = i0 + lane;
-        uint32_t n = 0, b = 0, spans = 0;
-        if (i < p.groups_per_xcd) {
-            b = fast_div(x + 8u * (uint32_t)i, p.div_hkv);
-            const int len = p.cu_q[b + 1] - p.cu_q[b];
-            spans = (uint32_t)(len + 127) >> 7;
-            n = spans * (uint32_t)p.items_per_span;
+    uint32_t base = 0;  // items of the groups before this round's 256
+    for (int i0 = 0; i0 < p.groups_per_xcd; i0 += 64 * PER) {
+        uint32_t n[PER], b[PER], spans[PER];
+        uint32_t sum = 0;
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int i = i0 + PER * lane + u;
+            n[u] = 0;
+            b[u] = 0;
+            spans[u] = 0;
+            if (i < p.groups_per_xcd) {
+                b[u] = fast_div(x + 8u * (uint32_t)i, p.div_hkv);
+                const int len = p.cu_q[b[u] + 1] - p.cu_q[b[u]];
+                spans[u] = (uint32_t)(len + 127) >> 7;
+                n[u] = spans[u] * (uint32_t)p.items_per_span;
+            }
+            sum += n[u];
         }
-        uint32_t incl = n;  // inclusive prefix sum over the lanes
+        uint32_t incl = sum;  // inclusive prefix sum over the lanes
 #pragma unroll
         for (int d = 1; d < 64; d <<= 1) {
             const uint32_t t = (uint32_t)__shfl_up((int)incl, d);
@@ -318,23 +329,32 @@ __device__ __forceinline__ WorkItem decode_packed(const AttnParams& p, uint32_t 
         }
         const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
         if (k < base + total) {
+            // the first lane whose groups reach past item k holds its group
             const uint64_t hit = __builtin_amdgcn_ballot_w64(base + incl > k);
             const int j = __builtin_ctzll(hit);
-            const uint32_t rem =
-                k - base - (__builtin_amdgcn_readlane(incl, j) - __builtin_amdgcn_readlane(n, j));
-            const uint32_t g = x + 8u * (uint32_t)(i0 + j);
-            const uint32_t bj = __builtin_amdgcn_readlane(b, j);
-            const uint32_t sj = __builtin_amdgcn_readlane(spans, j);
-            // inside the group: span from the top, head set, tile of the span
-            const uint32_t lo = rem & (uint32_t)(p.hp - 1), rest = rem >> p.hp_shift;
-            const uint32_t hi = fast_div(rest, p.div_group);
-            const int r = (int)(rest - hi * p.div_group.d);
-            const int qt_rev = (int)((hi << p.hp_shift) + lo);
-            it.b = (int)bj;
-            it.hkv = (int)(g - bj * p.div_hkv.d);
-            it.hq = it.hkv * p.group + (r << p.hp_shift);
-            it.qt = p.q_order ? qt_rev : (int)(sj << p.hp_shift) - 1 - qt_rev;
-            return it;
+            uint32_t before =
+                base + __builtin_amdgcn_readlane(incl, j) - __builtin_amdgcn_readlane(sum, j);
+#pragma unroll
+            for (int u = 0; u < PER; ++u) {
+                const uint32_t nu = __builtin_amdgcn_readlane(n[u], j);
+                if (k < before + nu) {
+                    const uint32_t rem = k - before;
+                    const uint32_t g = x + 8u * (uint32_t)(i0 + PER * j + u);
+                    const uint32_t bj = __builtin_amdgcn_readlane(b[u], j);
+                    const uint32_t sj = __builtin_amdgcn_readlane(spans[u], j);
+                    // inside the group: span from the top, head set, tile of the span
+                    const uint32_t lo = rem & (uint32_t)(p.hp - 1), rest = rem >> p.hp_shift;
+                    const uint32_t hi = fast_div(rest, p.div_group);
+                    const int r = (int)(rest - hi * p.div_group.d);
+                    const int qt_rev = (int)((hi << p.hp_shift) + lo);
+                    it.b = (int)bj;
+                    it.hkv = (int)(g - bj * p.div_hkv.d);
+                    it.hq = it.hkv * p.group + (r << p.hp_shift);
+                    it.qt = p.q_order ? qt_rev : (int)(sj << p.hp_shift) - 1 - qt_rev;
+                    return it;
+                }
+                before += nu;
+            }
         }
         base += total;
     }

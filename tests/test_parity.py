@@ -327,6 +327,11 @@ PACKED = [
     ("gqa2_window", 16, 8, 128, dict(mask=WINDOW, window_left=40, window_right=0),
      [129, 0, 77]),
     ("many_groups", 8, 8, 64, dict(mask=CAUSAL), "many"),
+    # more than 256 groups per XCD: several rounds of the decode's scan, with
+    # empty sequences at the round edges, and two kv heads of each sequence
+    # on one XCD
+    ("many_rounds", 8, 8, 64, dict(mask=CAUSAL), "rounds"),
+    ("many_rounds_hkv16", 32, 16, 128, dict(mask=CAUSAL), "rounds16"),
     ("global_window", 4, 1, 128, dict(mask=MASK_GLOBAL_WINDOW, window_left=16,
                                       window_right=16, num_global=3),
      [70, 1000, 0, 1, 130, 64, 33, 256] + [40] * 16),
@@ -351,6 +356,16 @@ def test_varlen_packed_grid(case):
         g = torch.Generator().manual_seed(9)
         lengths = torch.randint(0, 300, (130,), generator=g).tolist()
         lengths[7], lengths[8] = 0, 500
+    elif lengths == "rounds":  # 600 groups per XCD
+        g = torch.Generator().manual_seed(10)
+        lengths = torch.randint(0, 41, (600,), generator=g).tolist()
+        lengths[255] = lengths[256] = lengths[511] = lengths[512] = lengths[599] = 0
+        lengths[300] = 900
+    elif lengths == "rounds16":  # 300 groups per XCD, two per sequence
+        g = torch.Generator().manual_seed(12)
+        lengths = torch.randint(0, 30, (150,), generator=g).tolist()
+        lengths[127] = lengths[128] = 0
+        lengths[3] = 700
     assert packed_grid_applies(lengths, hq, hkv)
     log(f"[parity packed grid] {name} B={len(lengths)}")
     wl = Workload(name, "bf16", len(lengths), hq, hkv, 0, D, seed=27, varlen=True, **kw)
