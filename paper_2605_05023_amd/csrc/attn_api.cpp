@@ -465,13 +465,13 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     // Size of the packed grid of a bf16 variable-length batch walked one kv
     // group at a time per XCD (see below), or -1 where it cannot apply. An
     // XCD's groups hold at most ceil(hkv / 8) kv heads of any one sequence,
-    // so their spans number at most ceil(hkv / 8) * total_q / 128 + (groups
-    // per XCD).
+    // so their query tiles (128 / hp rows) number at most
+    // ceil(hkv / 8) * total_q * hp / 128 + (groups per XCD).
     int64_t packed = -1;
     if (d.dtype == ATTN_BF16 && varlen && p.map_mode == 1) {
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
         const int64_t per_seq = (d.num_kv_heads + 7) / 8;
-        packed = 8 * (per_seq * d.total_q / 128 + groups_per_xcd) * (group / hp) * hp;
+        packed = 8 * (per_seq * d.total_q * hp / 128 + groups_per_xcd) * (group / hp);
     }
     {
         const int64_t groups_per_xcd = ((int64_t)d.batch * d.num_kv_heads) / 8;
@@ -524,7 +524,7 @@ extern "C" int attn_fwd(const void* q, const void* k, const void* v, void* out, 
     p.grid = (int32_t)blocks;
     p.compact = 0;
     p.groups_per_xcd = 0;
-    p.items_per_span = gsets * hp;
+    p.items_per_tile = gsets;
     if (packed >= 0 && p.chunk == 1 && packed < blocks) {
         p.compact = 1;
         p.groups_per_xcd = (int32_t)(((int64_t)d.batch * d.num_kv_heads) / 8);

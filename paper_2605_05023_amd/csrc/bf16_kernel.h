@@ -290,10 +290,11 @@ struct Bool {
 // caches once per tile.
 // Packed variable-length grid (compact, with mode 1 and one kv group per
 // chunk): an XCD's work items are those of its groups g = x + 8 i in order i,
-// each group contributing only the query spans of its own sequence
-// (ceil(length / 128) spans of hp tiles, times its head sets), in the same
-// order inside the group as the padded grid, so no workgroup is spent on
-// tiles past a sequence's end. Every wave finds its group from the prefix
+// each group contributing only the query tiles of its own sequence
+// (ceil(length / tile rows) tiles, times its head sets), in the order of the
+// padded grid (128-row spans of hp tiles, the last span holding only the
+// tiles that have rows), so no workgroup is spent on tiles past a
+// sequence's end. Every wave finds its group from the prefix
 // sums of the item counts over the XCD's groups, 256 groups at a time (four
 // consecutive groups per lane, their length loads issued together, so a batch
 // of thousands of sequences waits on a quarter of the load round trips).
@@ -305,19 +306,20 @@ __device__ __forceinline__ WorkItem decode_packed(const AttnParams& p, uint32_t 
     const int lane = __lane_id();
     uint32_t base = 0;  // items of the groups before this round's 256
     for (int i0 = 0; i0 < p.groups_per_xcd; i0 += 64 * PER) {
-        uint32_t n[PER], b[PER], spans[PER];
+        uint32_t n[PER], b[PER], tiles[PER];
         uint32_t sum = 0;
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
             const int i = i0 + PER * lane + u;
             n[u] = 0;
             b[u] = 0;
-            spans[u] = 0;
+            tiles[u] = 0;
             if (i < p.groups_per_xcd) {
                 b[u] = fast_div(x + 8u * (uint32_t)i, p.div_hkv);
                 const int len = p.cu_q[b[u] + 1] - p.cu_q[b[u]];
-                spans[u] = (uint32_t)(len + 127) >> 7;
-                n[u] = spans[u] * (uint32_t)p.items_per_span;
+                // tiles of 128 / hp rows
+                tiles[u] = (uint32_t)(len + (127 >> p.hp_shift)) >> (7 - p.hp_shift);
+                n[u] = tiles[u] * (uint32_t)p.items_per_tile;
             }
             sum += n[u];
         }
@@ -341,16 +343,34 @@ __device__ __forceinline__ WorkItem decode_packed(const AttnParams& p, uint32_t 
                     const uint32_t rem = k - before;
                     const uint32_t g = x + 8u * (uint32_t)(i0 + PER * j + u);
                     const uint32_t bj = __builtin_amdgcn_readlane(b[u], j);
-                    const uint32_t sj = __builtin_amdgcn_readlane(spans[u], j);
-                    // inside the group: span from the top, head set, tile of the span
-                    const uint32_t lo = rem & (uint32_t)(p.hp - 1), rest = rem >> p.hp_shift;
-                    const uint32_t hi = fast_div(rest, p.div_group);
-                    const int r = (int)(rest - hi * p.div_group.d);
-                    const int qt_rev = (int)((hi << p.hp_shift) + lo);
+                    const uint32_t nt = __builtin_amdgcn_readlane(tiles[u], j);
+                    // inside the group: 128-row spans of hp tiles (the last
+                    // one holding t_top tiles), each span's items ordered by
+                    // head set, then tile; spans from the top (q_order 0) or
+                    // from the bottom (q_order 1), as in the padded grid
+                    const uint32_t hpu = (uint32_t)p.hp, gsets = p.div_group.d;
+                    const uint32_t sj = (nt + hpu - 1) >> p.hp_shift;       // spans, >= 1
+                    const uint32_t t_top = nt - ((sj - 1) << p.hp_shift);  // 1 .. hp
+                    const uint32_t top_first = p.q_order ? 0u : t_top * gsets;
+                    const uint32_t top_lo = p.q_order ? (sj - 1) * hpu * gsets : 0u;
+                    uint32_t r, qt;
+                    if (rem >= top_lo && rem < top_lo + t_top * gsets) {  // the last span
+                        const uint32_t e = rem - top_lo;
+                        r = e / t_top;
+                        const uint32_t lo = e - r * t_top;
+                        qt = ((sj - 1) << p.hp_shift) + (p.q_order ? lo : t_top - 1 - lo);
+                    } else {  // a full span
+                        const uint32_t e = rem - top_first;
+                        const uint32_t lo = e & (hpu - 1), rest = e >> p.hp_shift;
+                        const uint32_t hi = fast_div(rest, p.div_group);
+                        r = rest - hi * gsets;
+                        qt = p.q_order ? (hi << p.hp_shift) + lo
+                                       : ((sj - 2 - hi) << p.hp_shift) + (hpu - 1 - lo);
+                    }
                     it.b = (int)bj;
                     it.hkv = (int)(g - bj * p.div_hkv.d);
-                    it.hq = it.hkv * p.group + (r << p.hp_shift);
-                    it.qt = p.q_order ? qt_rev : (int)(sj << p.hp_shift) - 1 - qt_rev;
+                    it.hq = it.hkv * p.group + (int)(r << p.hp_shift);
+                    it.qt = (int)qt;
                     return it;
                 }
                 before += nu;

@@ -44,7 +44,7 @@ struct AttnParams {
     // only the query spans (128 rows) of each sequence (decode_packed)
     int32_t compact;
     int32_t groups_per_xcd;  // batch * hkv / 8
-    int32_t items_per_span;  // workgroups per 128-row span of a kv group: group / hp * hp
+    int32_t items_per_tile;  // workgroups per query tile of a kv group: group / hp
     int32_t grid;            // bf16: workgroups launched
     // bf16 listed global set: the first glob_items workgroups compute the rows
     // of G, wg_rows list entries each (glob_chunks per sequence and head set)

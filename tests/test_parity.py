@@ -345,7 +345,7 @@ def packed_grid_applies(lengths, hq, hkv):
     B, gsets = len(lengths), group // hp
     spans = -(-max(lengths) // 128)
     padded = spans * hp * (hq // hp) * B
-    packed = 8 * (-(-hkv // 8) * sum(lengths) // 128 + B * hkv // 8) * gsets * hp
+    packed = 8 * (-(-hkv // 8) * sum(lengths) * hp // 128 + B * hkv // 8) * gsets
     return packed < padded
 
 
