@@ -197,12 +197,13 @@ __device__ __forceinline__ void issue_load(char* lds_tile, __amdgpu_buffer_rsrc_
                                            uint32_t row_bytes, uint32_t lane_off, int wave, int p)
 {
     const uint32_t off = lane_off + (uint32_t)(j0 + p * T::ROWS_PER_LOAD) * row_bytes;
-    // Soft-cap kernels: an opaque wave offset makes each load form its LDS
-    // address from one register, where the compiler would otherwise keep one
-    // hoisted address per load and buffer, spill them from the scalar
-    // registers and reload them into the loop with vector instructions.
+    // Soft-cap and left-bounded softmax kernels: an opaque wave offset makes
+    // each load form its LDS address from one register, where the compiler
+    // would otherwise keep one hoisted address per load and buffer, spill
+    // them from the scalar registers and reload them into the loop with
+    // vector instructions.
     int wo = wave * 1024;
-    if constexpr (T::CAP != kCapOff) asm volatile("" : "+s"(wo));
+    if constexpr (T::CAP != kCapOff || (T::LEFT && T::SOFTMAX)) asm volatile("" : "+s"(wo));
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         rs, (lds_void*)(lds_tile + 4096 * p + wo), 16, off, 0, 0, 0);
 }
